@@ -1,0 +1,228 @@
+/*
+ * swapnet.h -- C ABI of the block-swapped inference engine for MI355X (gfx950).
+ *
+ * The engine runs a network whose weights do not fit a device-memory budget.
+ * It follows the problem statement of the SwapNet paper (Sec. 3, "Basic
+ * Idea"): given a budget b for a model of size s > b, the model is cut into
+ * ordered blocks of layers that are brought into memory and executed one by
+ * one.  On this hardware a swap-in is one DMA (hipMemcpyAsync) per slab from
+ * a pinned host image that already holds the device layout (the analogue of
+ * the paper's copy-free dispatch, Sec. 4.2.2), into a budget-sized HBM arena
+ * carved once at create time; parameters are bound by pointer into the arena
+ * (assembly by reference, Sec. 5.2); swap-out is write-back free (Sec. 4.1):
+ * a slab's range is reused as soon as its compute has finished.  The next
+ * slab is loaded on a copy stream while the current one computes (the m = 2
+ * parallel blocks of Sec. 6.2.2), ordered by hipEvents.
+ *
+ * Lifecycle:  sn_create -> sn_add_block (1..n times) -> sn_plan -> sn_infer*
+ *             -> sn_destroy.
+ *
+ * Errors: every call returns SN_OK (0) or a negative sn_status; nothing
+ * aborts.  sn_last_error(ctx) returns a description of the last failure on
+ * that context (sn_last_error(NULL): last failure of sn_create on this
+ * thread).  A context is not thread-safe; distinct contexts are independent.
+ *
+ * Numerics: fp16 weights and activations, fp32 accumulation; bias, residual,
+ * ReLU, SwiGLU, softmax, RMSNorm and RoPE evaluated in fp32; each kernel
+ * output rounded once to fp16 (logits stay fp32).  Kernels are deterministic
+ * and the reduction order of every output depends only on the layer, never
+ * on how the layer was split into slabs, so a swapped run is bit-identical
+ * to an all-resident run of the same network.
+ */
+#ifndef SWAPNET_H
+#define SWAPNET_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SN_API_VERSION 1
+
+typedef struct sn_ctx sn_ctx;
+
+/* Status codes (negative = failure). */
+enum sn_status {
+    SN_OK = 0,
+    SN_E_INVALID = -1,      /* malformed argument or layer descriptor          */
+    SN_E_STATE = -2,        /* call not allowed in the context's current state */
+    SN_E_INFEASIBLE = -3,   /* no slab partition satisfies the pair constraint */
+    SN_E_NOMEM = -4,        /* host or device allocation failed                */
+    SN_E_HIP = -5,          /* a HIP runtime call failed (text in last_error)  */
+    SN_E_UNSUPPORTED = -6   /* operation not available (e.g. host-only context)*/
+};
+
+/* Layer operators.  Activations live in "slots" (device buffers outside the
+ * budget).  Image networks keep activations as H x W x C_pad (channels
+ * innermost, C_pad = C rounded up to 8, padding channels zero); token
+ * networks keep [tokens][C].  Canonical weight layouts below are what the
+ * caller passes to sn_add_block; the engine repacks them once, at plan time,
+ * into the device layout held in the pinned image. */
+enum sn_op {
+    SN_OP_CONV2D = 1,           /* w [c_out][c_in][k][k], bias [c_out] (fp16).
+                                   Cross-correlation, zero padding, stride,
+                                   dilation; + bias (+ slot res) (ReLU)        */
+    SN_OP_LINEAR = 2,           /* w [c_out][c_in], optional bias [c_out].
+                                   y = W x + b (+ res) (ReLU).  SN_FLAG_SWIGLU:
+                                   w is [2F][c_in] = [W1; W3] stacked and the
+                                   output (F = c_out) is silu(W1 x) * (W3 x)  */
+    SN_OP_MAXPOOL = 3,          /* k x k window, stride, pad (never selected)  */
+    SN_OP_GAVGPOOL = 4,         /* mean over H x W -> [C]                      */
+    SN_OP_UPSAMPLE_BILINEAR = 5,/* integer factor `scale`, half-pixel centres,
+                                   edge-clamped (align_corners = false)        */
+    SN_OP_EMBED = 6,            /* table [c_out = vocab][c_in = d]; rows are
+                                   gathered by token id, never streamed       */
+    SN_OP_RMSNORM = 7,          /* gain [c_in]: v / sqrt(mean(v^2)+eps) * g    */
+    SN_OP_ATTENTION = 8         /* src = [T][3d] (q|k|v); RoPE (rotate-half,
+                                   theta), append k, v to the KV cache of
+                                   kv_layer, causal softmax(q k^T/sqrt(hd)) v  */
+};
+
+/* Layer flags. */
+enum sn_flag {
+    SN_FLAG_RELU = 1,           /* ReLU after bias/residual                    */
+    SN_FLAG_FLATTEN_CHW = 2,    /* linear over an H x W x C activation whose
+                                   canonical weight columns are in (C,H,W)
+                                   order (framework flatten order)             */
+    SN_FLAG_SWIGLU = 4,         /* see SN_OP_LINEAR                            */
+    SN_FLAG_OUT_F32 = 8,        /* output stored as fp32 (logits)              */
+    SN_FLAG_LAST_ROW = 16       /* token linear applied to the last row only   */
+};
+
+typedef struct sn_layer {
+    int32_t op;                 /* enum sn_op                                  */
+    int32_t src, res, dst;      /* activation slots; res = -1 for none.  The
+                                   network input is slot `src` of layer 0; the
+                                   output is slot `dst` of the last layer     */
+    int32_t c_in, c_out;        /* channels / features                         */
+    int32_t h_in, w_in;         /* input spatial size (image layers)          */
+    int32_t k, stride, pad, dilation;   /* conv / pool window                  */
+    int32_t scale;              /* upsample factor                             */
+    int32_t heads, head_dim;    /* attention                                   */
+    int32_t kv_layer;           /* attention: index of this layer's KV cache  */
+    int32_t max_tokens;         /* embed: tokens per call (activation rows)    */
+    int32_t max_seq;            /* attention: KV cache capacity (positions)    */
+    int32_t flags;              /* enum sn_flag                                */
+    float eps, theta;           /* rmsnorm epsilon, RoPE base                  */
+    int64_t w_off, w_bytes;     /* canonical weight (or gain / table) tensor,
+                                   byte offset and size in the block buffer;
+                                   w_bytes = 0 if the layer has none          */
+    int64_t b_off, b_bytes;     /* canonical bias; b_bytes = 0 if none        */
+} sn_layer;
+
+/* Create a context whose weight arena is `budget_bytes` of HBM, allocated
+ * here, once (no allocation happens per swap).  Also creates the copy and
+ * compute streams.  Returns NULL on failure (reason: sn_last_error(NULL)). */
+sn_ctx *sn_create(size_t budget_bytes);
+
+/* Context flags for sn_create_ex. */
+enum sn_create_flag {
+    SN_CREATE_HOST_ONLY = 1     /* no device calls at all: planning and
+                                   prepacking only, for inspection; the infer
+                                   calls return SN_E_UNSUPPORTED              */
+};
+sn_ctx *sn_create_ex(size_t budget_bytes, int flags);
+
+/* Register one block: `n_layers` descriptors (copied) and the block's
+ * weights in canonical layout (`weights`, `weight_bytes` bytes, copied; the
+ * caller may free both on return).  Blocks run in the order added.  A block
+ * is the user's partition unit (the paper's block, Sec. 3); the planner may
+ * split it further but never merges blocks.
+ * Errors: SN_E_INVALID (bad descriptor or out-of-range offsets),
+ * SN_E_STATE (after sn_plan). */
+int sn_add_block(sn_ctx *ctx, const sn_layer *layers, int n_layers,
+                 const void *weights, size_t weight_bytes);
+
+/* Plan and prepare: lower blocks to slabs so that every two consecutive
+ * slabs fit the budget together (the pair constraint s_i + s_{i+1} <= b of
+ * Sec. 6.2.2, Eq. 3, with the reserved share delta = 0 because activations
+ * live outside the budget); split a block at layer boundaries, then a layer
+ * by output channels, when needed; place slabs alternately at the two ends of
+ * the arena; build the pinned host image in device layout, slab after slab;
+ * allocate activations (and the KV cache) outside the budget.  If the whole
+ * image fits the budget it is uploaded once here and every inference runs
+ * all-resident.  Errors: SN_E_INFEASIBLE, SN_E_NOMEM, SN_E_HIP, SN_E_STATE. */
+int sn_plan(sn_ctx *ctx);
+
+/* Options (set before sn_plan unless noted). */
+enum sn_option {
+    SN_OPT_SPLIT_BUDGET = 1,    /* budget used for slab lowering (default: the
+                                   arena budget).  With an arena >= image and
+                                   a smaller split budget the run is resident
+                                   but has the slabs of the swapped plan      */
+    SN_OPT_TIMING = 2,          /* 1: record per-slab DMA / compute events
+                                   (may be set after plan)                    */
+    SN_OPT_MAX_SLAB = 3         /* cap on slab bytes (0 = none)               */
+};
+int sn_set_option(sn_ctx *ctx, int option, int64_t value);
+
+/* Image networks.  `input` is the fp16 input in canonical C x H x W order;
+ * `output` receives the last layer's output (C x H x W fp16 for spatial
+ * outputs, [c_out] for linear outputs, fp32 if SN_FLAG_OUT_F32).  Host
+ * pointers; synchronous. */
+int sn_infer(sn_ctx *ctx, const void *input, void *output);
+
+/* As sn_infer with device pointers; the work is ordered after prior work on
+ * `hip_stream` (a hipStream_t; NULL = the context's compute stream) and the
+ * output is ready when that stream reaches the point of return.  No host
+ * synchronisation. */
+int sn_infer_dev(sn_ctx *ctx, const void *d_input, void *d_output, void *hip_stream);
+
+/* Token networks (first layer SN_OP_EMBED).  Runs `n_ids` tokens (host
+ * int32 ids) at positions pos..pos+n_ids-1, appending to the KV cache, and
+ * writes the fp32 logits of the last token to `logits` (host, c_out floats).
+ * Synchronous. */
+int sn_infer_tokens(sn_ctx *ctx, const int32_t *ids, int n_ids, float *logits);
+
+/* Clear the token position (the KV cache is overwritten from position 0). */
+int sn_reset(sn_ctx *ctx);
+
+typedef struct sn_stats {
+    int64_t budget_bytes;       /* arena size                                  */
+    int64_t image_bytes;        /* pinned image (sum of slab bytes)            */
+    int64_t arena_high_water;   /* highest arena byte used by the placement    */
+    int64_t streamed_bytes;     /* weight bytes DMA'd per inference (0 when
+                                   resident)                                   */
+    int64_t activation_bytes;   /* device bytes outside the budget:           */
+    int64_t kv_bytes;           /*   activations, KV cache,                   */
+    int64_t table_bytes;        /*   host-side tables (plan, bindings)        */
+    int32_t n_slabs, n_pieces, n_layers, resident;
+    int64_t n_infers;
+    double last_ms;             /* last inference, host wall clock (ms)       */
+} sn_stats;
+int sn_get_stats(const sn_ctx *ctx, sn_stats *out);
+
+typedef struct sn_slab_info {
+    int64_t image_off;          /* byte offset in the pinned image            */
+    int64_t arena_off;          /* byte offset in the arena                   */
+    int64_t bytes;              /* slab bytes (tensors 256-byte aligned)      */
+    int32_t first_piece, n_pieces;
+    float t_in_ms, t_ex_ms;     /* last inference's DMA and compute time of
+                                   this slab (SN_OPT_TIMING), else 0          */
+    float t_in_start_ms, t_ex_start_ms; /* start times from inference start   */
+} sn_slab_info;
+int sn_get_slab(const sn_ctx *ctx, int i, sn_slab_info *out);
+
+typedef struct sn_piece_info {
+    int32_t layer;              /* global layer index                          */
+    int32_t c0, c1;             /* output channels [c0, c1) of that layer     */
+    int32_t kernel;             /* kernel variant chosen for the layer        */
+    int64_t w_off, b_off;       /* offsets in the slab (-1 if none)           */
+    int64_t w_bytes, b_bytes;
+} sn_piece_info;
+int sn_get_piece(const sn_ctx *ctx, int j, sn_piece_info *out);
+
+/* Pinned host image (after sn_plan): pointer and size, for inspection. */
+int sn_get_image(const sn_ctx *ctx, const void **ptr, size_t *bytes);
+
+const char *sn_last_error(const sn_ctx *ctx);
+
+/* Release everything (NULL-safe).  Waits for outstanding work first. */
+void sn_destroy(sn_ctx *ctx);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SWAPNET_H */

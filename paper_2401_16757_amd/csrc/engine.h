@@ -1,0 +1,79 @@
+// engine.h -- internal state of a swap-engine context (not part of the ABI).
+#pragma once
+#include <stdint.h>
+
+#include <string>
+#include <vector>
+
+#include "../../include/swapnet.h"
+
+namespace sn {
+
+constexpr int64_t kAlign = 256;   // alignment of every tensor and slab in the arena
+
+inline int64_t align_up(int64_t v, int64_t a = kAlign) { return (v + a - 1) / a * a; }
+inline int round8(int v) { return (v + 7) / 8 * 8; }
+
+// Shape of an activation slot: rows x cols fp16 (or fp32) elements.  Image
+// slots: rows = H*W, cols = Cp; token slots: rows = max tokens, cols = C.
+struct Slot {
+    bool used = false;
+    int h = 0, w = 0;          // spatial size (image slots)
+    int c = 0, cp = 0;         // channels, padded channels (cols)
+    int rows = 0;
+    int elem = 2;              // bytes per element
+    int first = 1 << 30;       // first layer writing it (-1: network input)
+    int last = -1;             // last layer reading it (L: network output)
+    int64_t bytes = 0, off = 0;
+};
+
+// One layer after validation, with its device-layout tensors (host copies
+// until the image is built).
+struct Layer {
+    sn_layer d{};
+    int block = 0;
+    bool token = false;        // part of a token (decoder) network
+    int out_h = 1, out_w = 1;
+    int cin_p = 0, cout_p = 0; // padded channel counts of src / dst
+    int K = 0;                 // device row length in halves (conv, linear)
+    int64_t units = 0;         // splittable output units (0: no weights)
+    int rows_per_unit = 1;     // weight rows per unit (2 for SwiGLU)
+    int64_t w_unit_bytes = 0;  // device weight bytes per unit
+    int64_t b_unit_bytes = 0;  // device bias bytes per unit
+    int kernel = -1;           // conv tile variant (image convs)
+    std::vector<uint16_t> w_dev, b_dev;  // device-layout tensors
+};
+
+// A piece = output units [u0, u1) of one layer, placed in one slab.
+struct Piece {
+    int layer = 0;
+    int64_t u0 = 0, u1 = 0;
+    int64_t w_off = -1, b_off = -1;   // slab-relative
+    int64_t w_bytes = 0, b_bytes = 0;
+};
+
+struct Slab {
+    std::vector<int> pieces;          // indices into Ctx::pieces (after lowering)
+    int64_t bytes = 0;
+    int64_t image_off = 0, arena_off = 0;
+};
+
+struct PlanResult {
+    std::vector<Piece> pieces;
+    std::vector<Slab> slabs;
+    bool resident = false;
+    int64_t image_bytes = 0, high_water = 0;
+};
+
+// Host-only planning (no device calls).
+int validate_layers(std::vector<Layer> &layers, int from, std::vector<Slot> &slots,
+                    std::string &err);
+int prepack_layer(Layer &L, const uint8_t *blob, size_t blob_bytes, std::string &err);
+int plan_slabs(const std::vector<Layer> &layers, int n_blocks, int64_t split_budget,
+               int64_t max_slab, PlanResult &out, std::string &err);
+int place_slabs(PlanResult &p, int64_t arena_budget, std::string &err);
+void assign_slot_offsets(std::vector<Slot> &slots, int64_t &total);
+void write_image(const std::vector<Layer> &layers, const PlanResult &p, uint8_t *image);
+void choose_kernels(std::vector<Layer> &layers);
+
+}  // namespace sn

@@ -1,0 +1,681 @@
+// engine.hip -- the swap engine and its C ABI (declared in include/swapnet.h).
+//
+// The swapping cycle of the paper (Sec. 3 workflow; Sec. 4 swap-in/out;
+// Sec. 5 assembly; Sec. 6.2.2 m = 2 parallel blocks), mapped onto one
+// MI355X:
+//   swap-in   one hipMemcpyAsync per slab, pinned image -> arena, on the copy
+//             stream, issued as soon as the slab two places back has finished
+//             computing (its arena range is then free);
+//   assemble  kernel arguments are arena base + the offsets fixed at plan
+//             time (no copies, no per-swap allocation);
+//   execute   the slab's layer pieces on the compute stream, after the
+//             slab's "loaded" event;
+//   swap-out  recording the slab's "done" event: nothing is freed or written
+//             back, the range is simply reused.
+#include <hip/hip_runtime.h>
+
+#include <chrono>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "engine.h"
+#include "kernels.h"
+
+using namespace sn;
+
+enum { ST_ADDING = 0, ST_PLANNED = 1 };
+
+struct sn_ctx {
+    int64_t budget = 0;
+    bool host_only = false;
+    int state = ST_ADDING;
+    std::string err;
+
+    std::vector<Layer> layers;
+    std::vector<Slot> slots;
+    int n_blocks = 0;
+    bool token = false;
+    int64_t split_budget = 0, max_slab = 0;
+    bool timing = false;
+
+    PlanResult plan;
+    std::vector<const void *> piece_w, piece_b;   // bound parameter pointers
+
+    // device state
+    int device = 0;
+    uint8_t *arena = nullptr;
+    hipStream_t copy_s = nullptr, comp_s = nullptr;
+    uint8_t *image = nullptr;          // pinned (device mode) or malloc (host-only)
+    uint8_t *act = nullptr;
+    int64_t act_bytes = 0;
+    uint8_t *kv = nullptr;
+    int64_t kv_bytes = 0;
+    int kv_layers = 0, max_seq = 0, d_model = 0, max_tokens = 0;
+    void *table_host = nullptr, *table_dev = nullptr;
+    int64_t table_bytes = 0;
+    int32_t *d_ids = nullptr;
+    float *q_scratch = nullptr;
+    void *in_stage = nullptr, *out_stage = nullptr;
+    int64_t in_bytes = 0, out_bytes = 0;
+    std::vector<hipEvent_t> loaded, done;
+    std::vector<hipEvent_t> t_in0, t_in1, t_ex0, t_ex1;
+    hipEvent_t t_start = nullptr;
+    bool have_prev = false;
+    int pos = 0;
+    int64_t n_infers = 0;
+    double last_ms = 0;
+    std::vector<float> slab_t_in, slab_t_ex, slab_t_in_start, slab_t_ex_start;
+};
+
+static thread_local std::string g_create_err;
+
+static int fail(sn_ctx *c, int code, const std::string &msg) {
+    if (c) c->err = msg;
+    return code;
+}
+
+#define HIP_TRY(ctx, call)                                                                       \
+    do {                                                                                         \
+        hipError_t e_ = (call);                                                                  \
+        if (e_ != hipSuccess)                                                                    \
+            return fail(ctx, SN_E_HIP, std::string(#call) + ": " + hipGetErrorString(e_));        \
+    } while (0)
+
+// ---------------------------------------------------------------------------
+// Create / add / plan
+// ---------------------------------------------------------------------------
+extern "C" sn_ctx *sn_create_ex(size_t budget_bytes, int flags) {
+    if (budget_bytes < (size_t)kAlign) {
+        g_create_err = "budget must be at least 256 bytes";
+        return nullptr;
+    }
+    sn_ctx *c = new (std::nothrow) sn_ctx();
+    if (!c) {
+        g_create_err = "out of host memory";
+        return nullptr;
+    }
+    c->budget = (int64_t)budget_bytes;
+    c->split_budget = c->budget;
+    c->host_only = flags & SN_CREATE_HOST_ONLY;
+    if (!c->host_only) {
+        hipError_t e = hipGetDevice(&c->device);
+        if (e == hipSuccess) e = hipMalloc((void **)&c->arena, (size_t)c->budget);
+        if (e == hipSuccess) e = hipStreamCreateWithFlags(&c->copy_s, hipStreamNonBlocking);
+        if (e == hipSuccess) e = hipStreamCreateWithFlags(&c->comp_s, hipStreamNonBlocking);
+        if (e != hipSuccess) {
+            g_create_err = std::string("device setup failed: ") + hipGetErrorString(e);
+            sn_destroy(c);
+            return nullptr;
+        }
+    }
+    return c;
+}
+
+extern "C" sn_ctx *sn_create(size_t budget_bytes) { return sn_create_ex(budget_bytes, 0); }
+
+extern "C" int sn_add_block(sn_ctx *c, const sn_layer *layers, int n_layers, const void *weights,
+                            size_t weight_bytes) {
+    if (!c) return SN_E_INVALID;
+    if (c->state != ST_ADDING) return fail(c, SN_E_STATE, "sn_add_block after sn_plan");
+    if (!layers || n_layers <= 0) return fail(c, SN_E_INVALID, "empty block");
+    if (weight_bytes && !weights) return fail(c, SN_E_INVALID, "weights is NULL");
+    const int from = (int)c->layers.size();
+    std::vector<Slot> saved = c->slots;
+    for (int i = 0; i < n_layers; ++i) {
+        Layer L;
+        L.d = layers[i];
+        L.block = c->n_blocks;
+        c->layers.push_back(std::move(L));
+    }
+    auto rollback = [&](int code, const std::string &m) {
+        c->layers.resize(from);
+        c->slots = saved;
+        return fail(c, code, m);
+    };
+    std::string err;
+    int rc = validate_layers(c->layers, from, c->slots, err);
+    if (rc) return rollback(rc, err);
+    for (int i = from; i < (int)c->layers.size(); ++i) {
+        try {
+            rc = prepack_layer(c->layers[i], (const uint8_t *)weights, weight_bytes, err);
+        } catch (const std::bad_alloc &) {
+            return rollback(SN_E_NOMEM, "out of host memory while prepacking");
+        }
+        if (rc) return rollback(rc, "layer " + std::to_string(i) + ": " + err);
+    }
+    c->token = c->layers[0].d.op == SN_OP_EMBED;
+    c->n_blocks++;
+    return SN_OK;
+}
+
+extern "C" int sn_set_option(sn_ctx *c, int option, int64_t value) {
+    if (!c) return SN_E_INVALID;
+    switch (option) {
+    case SN_OPT_SPLIT_BUDGET:
+        if (c->state != ST_ADDING) return fail(c, SN_E_STATE, "split budget is fixed at plan");
+        if (value < kAlign) return fail(c, SN_E_INVALID, "split budget too small");
+        c->split_budget = value;
+        return SN_OK;
+    case SN_OPT_TIMING:
+        c->timing = value != 0;
+        return SN_OK;
+    case SN_OPT_MAX_SLAB:
+        if (c->state != ST_ADDING) return fail(c, SN_E_STATE, "max slab is fixed at plan");
+        if (value < 0) return fail(c, SN_E_INVALID, "negative max slab");
+        c->max_slab = value;
+        return SN_OK;
+    default:
+        return fail(c, SN_E_INVALID, "unknown option");
+    }
+}
+
+static void choose_layer_kernels(sn_ctx *c) {
+    for (Layer &L : c->layers) {
+        if (L.d.op != SN_OP_CONV2D) continue;
+        const bool is1x1 = L.d.k == 1 && L.d.pad == 0;
+        L.kernel = conv_kernel_choice(L.out_h * L.out_w, L.d.c_out, L.K, is1x1);
+    }
+}
+
+static uint8_t *slot_ptr(sn_ctx *c, int id) { return c->act + c->slots[id].off; }
+
+extern "C" int sn_plan(sn_ctx *c) {
+    if (!c) return SN_E_INVALID;
+    if (c->state != ST_ADDING) return fail(c, SN_E_STATE, "sn_plan called twice");
+    if (c->layers.empty()) return fail(c, SN_E_STATE, "no blocks added");
+    std::string err;
+    const int L = (int)c->layers.size();
+    // the network output stays live to the end
+    c->slots[c->layers[L - 1].d.dst].last = L;
+    int rc = plan_slabs(c->layers, c->n_blocks, c->split_budget, c->max_slab, c->plan, err);
+    if (rc) return fail(c, rc, err);
+    rc = place_slabs(c->plan, c->budget, err);
+    if (rc) return fail(c, rc, err);
+    choose_layer_kernels(c);
+
+    // token-network geometry
+    if (c->token) {
+        c->max_tokens = c->layers[0].d.max_tokens;
+        c->d_model = c->layers[0].d.c_in;
+        for (const Layer &Ly : c->layers) {
+            if (Ly.d.op != SN_OP_ATTENTION) continue;
+            c->kv_layers = std::max(c->kv_layers, Ly.d.kv_layer + 1);
+            if (c->max_seq && c->max_seq != Ly.d.max_seq)
+                return fail(c, SN_E_INVALID, "attention layers disagree on max_seq");
+            c->max_seq = Ly.d.max_seq;
+        }
+    }
+    assign_slot_offsets(c->slots, c->act_bytes);
+
+    // network input / output sizes
+    const Layer &first = c->layers[0];
+    const Slot &outs = c->slots[c->layers[L - 1].d.dst];
+    if (!c->token) {
+        const Slot &ins = c->slots[first.d.src];
+        c->in_bytes = (int64_t)ins.c * ins.h * ins.w * 2;
+    }
+    c->out_bytes = (int64_t)outs.c * outs.h * outs.w * outs.elem;
+    if (c->token) c->out_bytes = (int64_t)outs.c * outs.elem;
+
+    if (c->host_only) {
+        c->image = (uint8_t *)malloc((size_t)std::max<int64_t>(c->plan.image_bytes, 1));
+        if (!c->image) return fail(c, SN_E_NOMEM, "host image allocation failed");
+        write_image(c->layers, c->plan, c->image);
+        if (c->token) {
+            c->table_bytes = (int64_t)first.w_dev.size() * 2;
+        }
+        for (Layer &Ly : c->layers) {
+            std::vector<uint16_t>().swap(Ly.w_dev);
+            std::vector<uint16_t>().swap(Ly.b_dev);
+        }
+        c->state = ST_PLANNED;
+        return SN_OK;
+    }
+
+    HIP_TRY(c, hipHostMalloc((void **)&c->image, (size_t)std::max<int64_t>(c->plan.image_bytes, 1),
+                             hipHostMallocDefault));
+    write_image(c->layers, c->plan, c->image);
+    HIP_TRY(c, hipMalloc((void **)&c->act, (size_t)std::max<int64_t>(c->act_bytes, kAlign)));
+    HIP_TRY(c, hipMemset(c->act, 0, (size_t)std::max<int64_t>(c->act_bytes, kAlign)));
+    if (c->token) {
+        c->table_bytes = (int64_t)first.w_dev.size() * 2;
+        HIP_TRY(c, hipHostMalloc(&c->table_host, (size_t)c->table_bytes, hipHostMallocMapped));
+        memcpy(c->table_host, first.w_dev.data(), (size_t)c->table_bytes);
+        HIP_TRY(c, hipHostGetDevicePointer(&c->table_dev, c->table_host, 0));
+        c->kv_bytes = 2ll * c->kv_layers * c->max_seq * c->d_model * 2;
+        HIP_TRY(c, hipMalloc((void **)&c->kv, (size_t)std::max<int64_t>(c->kv_bytes, kAlign)));
+        HIP_TRY(c, hipMalloc((void **)&c->d_ids, (size_t)c->max_tokens * 4));
+        HIP_TRY(c, hipMalloc((void **)&c->q_scratch, (size_t)c->max_tokens * c->d_model * 4));
+    } else {
+        HIP_TRY(c, hipMalloc(&c->in_stage, (size_t)c->in_bytes));
+    }
+    HIP_TRY(c, hipMalloc(&c->out_stage, (size_t)std::max<int64_t>(c->out_bytes, 4)));
+    for (Layer &Ly : c->layers) {
+        std::vector<uint16_t>().swap(Ly.w_dev);
+        std::vector<uint16_t>().swap(Ly.b_dev);
+    }
+
+    // binding table (assembly by reference): parameter pointers into the arena
+    const int np = (int)c->plan.pieces.size();
+    c->piece_w.assign(np, nullptr);
+    c->piece_b.assign(np, nullptr);
+    for (const Slab &s : c->plan.slabs)
+        for (int pi : s.pieces) {
+            const Piece &p = c->plan.pieces[pi];
+            if (p.w_bytes) c->piece_w[pi] = c->arena + s.arena_off + p.w_off;
+            if (p.b_bytes) c->piece_b[pi] = c->arena + s.arena_off + p.b_off;
+        }
+
+    const int ns = (int)c->plan.slabs.size();
+    c->loaded.assign(ns, nullptr);
+    c->done.assign(ns, nullptr);
+    for (int i = 0; i < ns; ++i) {
+        HIP_TRY(c, hipEventCreateWithFlags(&c->loaded[i], hipEventDisableTiming));
+        HIP_TRY(c, hipEventCreateWithFlags(&c->done[i], hipEventDisableTiming));
+    }
+    c->t_in0.assign(ns, nullptr);
+    c->t_in1.assign(ns, nullptr);
+    c->t_ex0.assign(ns, nullptr);
+    c->t_ex1.assign(ns, nullptr);
+    for (int i = 0; i < ns; ++i) {
+        HIP_TRY(c, hipEventCreate(&c->t_in0[i]));
+        HIP_TRY(c, hipEventCreate(&c->t_in1[i]));
+        HIP_TRY(c, hipEventCreate(&c->t_ex0[i]));
+        HIP_TRY(c, hipEventCreate(&c->t_ex1[i]));
+    }
+    HIP_TRY(c, hipEventCreate(&c->t_start));
+    c->slab_t_in.assign(ns, 0.f);
+    c->slab_t_ex.assign(ns, 0.f);
+    c->slab_t_in_start.assign(ns, 0.f);
+    c->slab_t_ex_start.assign(ns, 0.f);
+
+    if (c->plan.resident) {
+        // everything fits: one upload now, no swapping per inference
+        for (const Slab &s : c->plan.slabs)
+            if (s.bytes)
+                HIP_TRY(c, hipMemcpyAsync(c->arena + s.arena_off, c->image + s.image_off,
+                                          (size_t)s.bytes, hipMemcpyHostToDevice, c->copy_s));
+        HIP_TRY(c, hipStreamSynchronize(c->copy_s));
+    }
+    c->state = ST_PLANNED;
+    return SN_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Execution
+// ---------------------------------------------------------------------------
+static int run_piece(sn_ctx *c, int pi, int n_tok, hipStream_t s) {
+    const Piece &p = c->plan.pieces[pi];
+    const Layer &L = c->layers[p.layer];
+    const sn_layer &d = L.d;
+    hipError_t e = hipSuccess;
+    switch (d.op) {
+    case SN_OP_CONV2D: {
+        ConvArgs a{};
+        a.x = slot_ptr(c, d.src);
+        a.w = c->piece_w[pi];
+        a.bias = c->piece_b[pi];
+        a.res = d.res >= 0 ? slot_ptr(c, d.res) : nullptr;
+        a.y = slot_ptr(c, d.dst);
+        a.H = d.h_in;
+        a.W = d.w_in;
+        a.Cin_p = L.cin_p;
+        a.Ho = L.out_h;
+        a.Wo = L.out_w;
+        a.kh = a.kw = d.k;
+        a.stride = d.stride;
+        a.pad = d.pad;
+        a.dil = d.dilation;
+        a.K = L.K;
+        a.M = L.out_h * L.out_w;
+        a.N = (int)(p.u1 - p.u0);
+        a.n0 = (int)p.u0;
+        a.ldy = L.cout_p;
+        a.n_zero_end = p.u1 == L.units ? L.cout_p : (int)p.u1;
+        a.relu = (d.flags & SN_FLAG_RELU) ? 1 : 0;
+        e = launch_conv(L.kernel, a, s);
+        break;
+    }
+    case SN_OP_LINEAR: {
+        const int M = L.token ? ((d.flags & SN_FLAG_LAST_ROW) ? 1 : n_tok) : 1;
+        const uint8_t *x = slot_ptr(c, d.src);
+        if (L.token && (d.flags & SN_FLAG_LAST_ROW)) x += (int64_t)(n_tok - 1) * L.K * 2;
+        const bool swiglu = d.flags & SN_FLAG_SWIGLU;
+        const int rows = (int)(p.u1 - p.u0) * L.rows_per_unit;
+        if (M == 1) {
+            GemvArgs g{};
+            g.x = x;
+            g.w = c->piece_w[pi];
+            g.bias = c->piece_b[pi];
+            g.res = d.res >= 0 ? slot_ptr(c, d.res) : nullptr;
+            g.y = slot_ptr(c, d.dst);
+            g.rows = rows;
+            g.K = L.K;
+            g.n0 = (int)p.u0;
+            g.relu = (d.flags & SN_FLAG_RELU) ? 1 : 0;
+            g.swiglu = swiglu;
+            g.out_f32 = (d.flags & SN_FLAG_OUT_F32) ? 1 : 0;
+            // the last piece also zeroes the padding channels of the output
+            g.zero_end = (!L.token && p.u1 == L.units) ? L.cout_p : 0;
+            e = launch_gemv(g, s);
+        } else {
+            if (d.flags & SN_FLAG_OUT_F32) return fail(c, SN_E_UNSUPPORTED, "fp32 output needs M = 1");
+            ConvArgs a{};
+            a.x = x;
+            a.w = c->piece_w[pi];
+            a.bias = c->piece_b[pi];
+            a.res = d.res >= 0 ? slot_ptr(c, d.res) : nullptr;
+            a.y = slot_ptr(c, d.dst);
+            a.H = M;
+            a.W = 1;
+            a.Cin_p = L.K;
+            a.Ho = M;
+            a.Wo = 1;
+            a.kh = a.kw = 1;
+            a.stride = 1;
+            a.pad = 0;
+            a.dil = 1;
+            a.K = L.K;
+            a.M = M;
+            a.N = rows;
+            a.n0 = (int)p.u0;
+            a.ldy = d.c_out;
+            a.n_zero_end = 0;
+            a.relu = (d.flags & SN_FLAG_RELU) ? 1 : 0;
+            a.swiglu = swiglu;
+            // tile chosen from the whole layer, never from the piece
+            int kern = conv_kernel_choice(M, (int)L.units * L.rows_per_unit, L.K, true);
+            e = launch_conv(kern, a, s);
+        }
+        break;
+    }
+    case SN_OP_MAXPOOL:
+        e = launch_maxpool(slot_ptr(c, d.src), slot_ptr(c, d.dst), d.h_in, d.w_in, L.cin_p, L.out_h,
+                           L.out_w, d.k, d.stride, d.pad, s);
+        break;
+    case SN_OP_GAVGPOOL:
+        e = launch_gavgpool(slot_ptr(c, d.src), slot_ptr(c, d.dst), d.h_in * d.w_in, L.cin_p, s);
+        break;
+    case SN_OP_UPSAMPLE_BILINEAR:
+        e = launch_upsample(slot_ptr(c, d.src), slot_ptr(c, d.dst), d.h_in, d.w_in, L.cin_p, d.scale, s);
+        break;
+    case SN_OP_EMBED:
+        e = launch_embed(c->d_ids, c->table_dev, slot_ptr(c, d.dst), n_tok, d.c_in, s);
+        break;
+    case SN_OP_RMSNORM:
+        e = launch_rmsnorm(slot_ptr(c, d.src), c->piece_w[pi], slot_ptr(c, d.dst), n_tok, d.c_in,
+                           d.eps, s);
+        break;
+    case SN_OP_ATTENTION: {
+        const int64_t per = (int64_t)c->max_seq * c->d_model * 2;
+        uint8_t *kc = c->kv + (int64_t)d.kv_layer * 2 * per;
+        e = launch_attention(slot_ptr(c, d.src), kc, kc + per, c->q_scratch, slot_ptr(c, d.dst),
+                             n_tok, c->pos, d.heads, d.head_dim, d.theta, s);
+        break;
+    }
+    default:
+        return fail(c, SN_E_INVALID, "unknown op at run time");
+    }
+    if (e != hipSuccess)
+        return fail(c, SN_E_HIP, std::string("kernel launch (layer ") + std::to_string(p.layer) +
+                                     "): " + hipGetErrorString(e));
+    return SN_OK;
+}
+
+// Swap-in of slab i on the copy stream.  Slab i reuses the arena range of
+// slab i-2 (two-ended placement), so it waits for that slab's compute.  The
+// first two slabs of an inference wait for the last slab of the previous
+// inference that used the same end of the arena.
+static int enqueue_copy(sn_ctx *c, int i) {
+    const Slab &s = c->plan.slabs[i];
+    const int ns = (int)c->plan.slabs.size();
+    if (i >= 2) {
+        HIP_TRY(c, hipStreamWaitEvent(c->copy_s, c->done[i - 2], 0));
+    } else if (c->have_prev) {
+        int last_same = (ns - 1) - (((ns - 1) - i) % 2);
+        HIP_TRY(c, hipStreamWaitEvent(c->copy_s, c->done[last_same], 0));
+    }
+    if (c->timing) HIP_TRY(c, hipEventRecord(c->t_in0[i], c->copy_s));
+    if (s.bytes)
+        HIP_TRY(c, hipMemcpyAsync(c->arena + s.arena_off, c->image + s.image_off, (size_t)s.bytes,
+                                  hipMemcpyHostToDevice, c->copy_s));
+    if (c->timing) HIP_TRY(c, hipEventRecord(c->t_in1[i], c->copy_s));
+    HIP_TRY(c, hipEventRecord(c->loaded[i], c->copy_s));
+    return SN_OK;
+}
+
+static int run_network(sn_ctx *c, int n_tok, hipStream_t cs) {
+    const int ns = (int)c->plan.slabs.size();
+    const bool swap = !c->plan.resident;
+    int rc;
+    if (c->timing) HIP_TRY(c, hipEventRecord(c->t_start, cs));
+    if (swap) {
+        // the copy stream must not run ahead of work the caller queued earlier
+        // on `cs` that may still read activations of a previous inference
+        for (int i = 0; i < std::min(ns, 2); ++i)
+            if ((rc = enqueue_copy(c, i))) return rc;
+    }
+    for (int i = 0; i < ns; ++i) {
+        const Slab &s = c->plan.slabs[i];
+        if (swap) HIP_TRY(c, hipStreamWaitEvent(cs, c->loaded[i], 0));
+        if (c->timing) HIP_TRY(c, hipEventRecord(c->t_ex0[i], cs));
+        for (int pi : s.pieces)
+            if ((rc = run_piece(c, pi, n_tok, cs))) return rc;
+        if (c->timing) HIP_TRY(c, hipEventRecord(c->t_ex1[i], cs));
+        HIP_TRY(c, hipEventRecord(c->done[i], cs));
+        if (swap && i + 2 < ns)
+            if ((rc = enqueue_copy(c, i + 2))) return rc;
+    }
+    c->have_prev = true;
+    return SN_OK;
+}
+
+static void collect_timing(sn_ctx *c) {
+    if (!c->timing) return;
+    const int ns = (int)c->plan.slabs.size();
+    for (int i = 0; i < ns; ++i) {
+        float a = 0, b = 0, x = 0, y = 0;
+        if (!c->plan.resident) {
+            hipEventElapsedTime(&a, c->t_in0[i], c->t_in1[i]);
+            hipEventElapsedTime(&x, c->t_start, c->t_in0[i]);
+        }
+        hipEventElapsedTime(&b, c->t_ex0[i], c->t_ex1[i]);
+        hipEventElapsedTime(&y, c->t_start, c->t_ex0[i]);
+        c->slab_t_in[i] = a;
+        c->slab_t_ex[i] = b;
+        c->slab_t_in_start[i] = x;
+        c->slab_t_ex_start[i] = y;
+    }
+}
+
+static int check_ready(sn_ctx *c, bool token) {
+    if (!c) return SN_E_INVALID;
+    if (c->state != ST_PLANNED) return fail(c, SN_E_STATE, "inference before sn_plan");
+    if (c->host_only) return fail(c, SN_E_UNSUPPORTED, "host-only context cannot run");
+    if (c->token != token)
+        return fail(c, SN_E_UNSUPPORTED, token ? "not a token network" : "token network: use sn_infer_tokens");
+    return SN_OK;
+}
+
+static int infer_dev_impl(sn_ctx *c, const void *d_in, void *d_out, hipStream_t cs) {
+    const Layer &first = c->layers[0];
+    const Slot &ins = c->slots[first.d.src];
+    hipError_t e;
+    if (ins.h * ins.w > 1 || ins.cp != ins.c)
+        e = launch_chw_to_hwc(d_in, slot_ptr(c, first.d.src), ins.c, ins.h, ins.w, ins.cp, cs);
+    else
+        e = hipMemcpyAsync(slot_ptr(c, first.d.src), d_in, (size_t)ins.c * 2, hipMemcpyDeviceToDevice, cs);
+    if (e != hipSuccess) return fail(c, SN_E_HIP, std::string("input: ") + hipGetErrorString(e));
+    int rc = run_network(c, 1, cs);
+    if (rc) return rc;
+    const Slot &o = c->slots[c->layers.back().d.dst];
+    if (o.h * o.w > 1)
+        e = launch_hwc_to_chw(slot_ptr(c, c->layers.back().d.dst), d_out, o.c, o.h, o.w, o.cp, cs);
+    else
+        e = hipMemcpyAsync(d_out, slot_ptr(c, c->layers.back().d.dst), (size_t)o.c * o.elem,
+                           hipMemcpyDeviceToDevice, cs);
+    if (e != hipSuccess) return fail(c, SN_E_HIP, std::string("output: ") + hipGetErrorString(e));
+    c->n_infers++;
+    return SN_OK;
+}
+
+extern "C" int sn_infer_dev(sn_ctx *c, const void *d_in, void *d_out, void *hip_stream) {
+    int rc = check_ready(c, false);
+    if (rc) return rc;
+    if (!d_in || !d_out) return fail(c, SN_E_INVALID, "NULL buffer");
+    hipStream_t cs = hip_stream ? (hipStream_t)hip_stream : c->comp_s;
+    return infer_dev_impl(c, d_in, d_out, cs);
+}
+
+extern "C" int sn_infer(sn_ctx *c, const void *input, void *output) {
+    int rc = check_ready(c, false);
+    if (rc) return rc;
+    if (!input || !output) return fail(c, SN_E_INVALID, "NULL buffer");
+    auto t0 = std::chrono::steady_clock::now();
+    HIP_TRY(c, hipMemcpyAsync(c->in_stage, input, (size_t)c->in_bytes, hipMemcpyHostToDevice, c->comp_s));
+    rc = infer_dev_impl(c, c->in_stage, c->out_stage, c->comp_s);
+    if (rc) {
+        hipStreamSynchronize(c->comp_s);
+        hipStreamSynchronize(c->copy_s);
+        return rc;
+    }
+    HIP_TRY(c, hipMemcpyAsync(output, c->out_stage, (size_t)c->out_bytes, hipMemcpyDeviceToHost, c->comp_s));
+    HIP_TRY(c, hipStreamSynchronize(c->comp_s));
+    collect_timing(c);
+    c->last_ms = std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();
+    return SN_OK;
+}
+
+extern "C" int sn_infer_tokens(sn_ctx *c, const int32_t *ids, int n_ids, float *logits) {
+    int rc = check_ready(c, true);
+    if (rc) return rc;
+    if (!ids || !logits) return fail(c, SN_E_INVALID, "NULL buffer");
+    if (n_ids <= 0 || n_ids > c->max_tokens)
+        return fail(c, SN_E_INVALID, "n_ids must be in [1, max_tokens]");
+    if (c->pos + n_ids > c->max_seq) return fail(c, SN_E_INVALID, "KV cache full (max_seq reached)");
+    const int vocab = c->layers[0].d.c_out;
+    for (int i = 0; i < n_ids; ++i)
+        if (ids[i] < 0 || ids[i] >= vocab) return fail(c, SN_E_INVALID, "token id out of range");
+    auto t0 = std::chrono::steady_clock::now();
+    hipStream_t cs = c->comp_s;
+    HIP_TRY(c, hipMemcpyAsync(c->d_ids, ids, (size_t)n_ids * 4, hipMemcpyHostToDevice, cs));
+    rc = run_network(c, n_ids, cs);
+    if (rc) {
+        hipStreamSynchronize(cs);
+        hipStreamSynchronize(c->copy_s);
+        return rc;
+    }
+    HIP_TRY(c, hipMemcpyAsync(logits, slot_ptr(c, c->layers.back().d.dst), (size_t)c->out_bytes,
+                              hipMemcpyDeviceToHost, cs));
+    HIP_TRY(c, hipStreamSynchronize(cs));
+    collect_timing(c);
+    c->pos += n_ids;
+    c->n_infers++;
+    c->last_ms = std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();
+    return SN_OK;
+}
+
+extern "C" int sn_reset(sn_ctx *c) {
+    if (!c) return SN_E_INVALID;
+    if (c->state != ST_PLANNED) return fail(c, SN_E_STATE, "sn_reset before sn_plan");
+    c->pos = 0;
+    return SN_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Introspection
+// ---------------------------------------------------------------------------
+extern "C" int sn_get_stats(const sn_ctx *c, sn_stats *o) {
+    if (!c || !o) return SN_E_INVALID;
+    memset(o, 0, sizeof(*o));
+    o->budget_bytes = c->budget;
+    o->n_layers = (int32_t)c->layers.size();
+    if (c->state != ST_PLANNED) return SN_OK;
+    o->image_bytes = c->plan.image_bytes;
+    o->arena_high_water = c->plan.high_water;
+    o->streamed_bytes = c->plan.resident ? 0 : c->plan.image_bytes;
+    o->activation_bytes = c->act_bytes;
+    o->kv_bytes = c->kv_bytes;
+    o->table_bytes = (int64_t)(c->plan.pieces.size() * sizeof(Piece) + c->plan.slabs.size() * sizeof(Slab) +
+                               c->piece_w.size() * 2 * sizeof(void *) + c->layers.size() * sizeof(Layer));
+    o->n_slabs = (int32_t)c->plan.slabs.size();
+    o->n_pieces = (int32_t)c->plan.pieces.size();
+    o->resident = c->plan.resident ? 1 : 0;
+    o->n_infers = c->n_infers;
+    o->last_ms = c->last_ms;
+    return SN_OK;
+}
+
+extern "C" int sn_get_slab(const sn_ctx *c, int i, sn_slab_info *o) {
+    if (!c || !o) return SN_E_INVALID;
+    if (c->state != ST_PLANNED) return SN_E_STATE;
+    if (i < 0 || i >= (int)c->plan.slabs.size()) return SN_E_INVALID;
+    const Slab &s = c->plan.slabs[i];
+    memset(o, 0, sizeof(*o));
+    o->image_off = s.image_off;
+    o->arena_off = s.arena_off;
+    o->bytes = s.bytes;
+    o->first_piece = s.pieces.empty() ? -1 : s.pieces.front();
+    o->n_pieces = (int32_t)s.pieces.size();
+    if (i < (int)c->slab_t_in.size()) {
+        o->t_in_ms = c->slab_t_in[i];
+        o->t_ex_ms = c->slab_t_ex[i];
+        o->t_in_start_ms = c->slab_t_in_start[i];
+        o->t_ex_start_ms = c->slab_t_ex_start[i];
+    }
+    return SN_OK;
+}
+
+extern "C" int sn_get_piece(const sn_ctx *c, int j, sn_piece_info *o) {
+    if (!c || !o) return SN_E_INVALID;
+    if (c->state != ST_PLANNED) return SN_E_STATE;
+    if (j < 0 || j >= (int)c->plan.pieces.size()) return SN_E_INVALID;
+    const Piece &p = c->plan.pieces[j];
+    o->layer = p.layer;
+    o->c0 = (int32_t)p.u0;
+    o->c1 = (int32_t)p.u1;
+    o->kernel = c->layers[p.layer].kernel;
+    o->w_off = p.w_off;
+    o->b_off = p.b_off;
+    o->w_bytes = p.w_bytes;
+    o->b_bytes = p.b_bytes;
+    return SN_OK;
+}
+
+extern "C" int sn_get_image(const sn_ctx *c, const void **ptr, size_t *bytes) {
+    if (!c || !ptr || !bytes) return SN_E_INVALID;
+    if (c->state != ST_PLANNED) return SN_E_STATE;
+    *ptr = c->image;
+    *bytes = (size_t)c->plan.image_bytes;
+    return SN_OK;
+}
+
+extern "C" const char *sn_last_error(const sn_ctx *c) {
+    if (!c) return g_create_err.c_str();
+    return c->err.c_str();
+}
+
+extern "C" void sn_destroy(sn_ctx *c) {
+    if (!c) return;
+    if (!c->host_only) {
+        if (c->comp_s) hipStreamSynchronize(c->comp_s);
+        if (c->copy_s) hipStreamSynchronize(c->copy_s);
+        for (auto *v : {&c->loaded, &c->done, &c->t_in0, &c->t_in1, &c->t_ex0, &c->t_ex1})
+            for (hipEvent_t e : *v)
+                if (e) hipEventDestroy(e);
+        if (c->t_start) hipEventDestroy(c->t_start);
+        if (c->image) hipHostFree(c->image);
+        if (c->table_host) hipHostFree(c->table_host);
+        for (void *p : {(void *)c->arena, (void *)c->act, (void *)c->kv, (void *)c->d_ids,
+                        (void *)c->q_scratch, c->in_stage, c->out_stage})
+            if (p) hipFree(p);
+        if (c->copy_s) hipStreamDestroy(c->copy_s);
+        if (c->comp_s) hipStreamDestroy(c->comp_s);
+    } else {
+        free(c->image);
+    }
+    delete c;
+}

@@ -1,0 +1,74 @@
+// kernels.h -- launch interface of the gfx950 kernels used by the swap engine.
+//
+// All tensors are fp16 (stored as _Float16 on the device) unless noted.
+// Activations of image networks are H x W x Cp (channels innermost, Cp a
+// multiple of 8); token networks use [T][C].  Weights are in the device
+// layout written by the planner: one row per output channel, K contiguous.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace sn {
+
+// Implicit-GEMM convolution / token GEMM on MFMA.  Output element
+// (m = output pixel or token, n = output channel) is
+//   sum_k A[m][k] * W[n][k]  with k = (r, s, ci) over the kh x kw x Cin_p window,
+// plus bias, plus residual, then ReLU, rounded once to fp16.
+struct ConvArgs {
+    const void *x;      // input activation, H x W x Cin_p
+    const void *w;      // piece weights, [N rows][K] (rows interleaved gate/up for SwiGLU)
+    const void *bias;   // piece bias [N] or null
+    const void *res;    // residual activation (same layout as y) or null
+    void *y;            // output activation base (channel stride ldy)
+    int H, W, Cin_p;
+    int Ho, Wo;
+    int kh, kw, stride, pad, dil;
+    int K;              // kh * kw * Cin_p
+    int M;              // Ho * Wo (or tokens)
+    int N;              // weight rows in this piece
+    int n0;             // first output channel of the piece (in output units)
+    int ldy;            // channel stride of y and res
+    int n_zero_end;     // zero output channels [n0 + units, n_zero_end) (padding)
+    int relu, swiglu;
+};
+
+// Matrix-vector product for batch-1 linear layers (HBM-bound):
+//   y[n0 + n] = sum_k W[n][k] x[k] (+ b[n]) (+ res[n0 + n]) (ReLU)
+// SwiGLU: weight rows come in (gate, up) pairs; output unit j is
+//   silu(row 2j . x) * (row 2j+1 . x).
+struct GemvArgs {
+    const void *x;
+    const void *w;
+    const void *bias;
+    const void *res;
+    void *y;
+    int rows;           // weight rows in this piece
+    int K;              // row length (multiple of 8)
+    int n0;             // first output unit of the piece
+    int relu, swiglu, out_f32;
+    int zero_end;       // if > n0 + units: zero outputs [n0 + units, zero_end)
+};
+
+int conv_kernel_choice(int M, int N, int K, bool is1x1);
+int conv_kernel_count();
+const char *conv_kernel_name(int id);
+hipError_t launch_conv(int kernel, const ConvArgs &a, hipStream_t s);
+hipError_t launch_gemv(const GemvArgs &a, hipStream_t s);
+
+hipError_t launch_maxpool(const void *x, void *y, int H, int W, int Cp, int Ho, int Wo, int k,
+                          int stride, int pad, hipStream_t s);
+hipError_t launch_gavgpool(const void *x, void *y, int HW, int Cp, hipStream_t s);
+hipError_t launch_upsample(const void *x, void *y, int H, int W, int Cp, int scale, hipStream_t s);
+hipError_t launch_chw_to_hwc(const void *x, void *y, int C, int H, int W, int Cp, hipStream_t s);
+hipError_t launch_hwc_to_chw(const void *x, void *y, int C, int H, int W, int Cp, hipStream_t s);
+
+hipError_t launch_embed(const int32_t *ids, const void *table, void *y, int T, int d, hipStream_t s);
+hipError_t launch_rmsnorm(const void *x, const void *gain, void *y, int T, int d, float eps,
+                          hipStream_t s);
+// RoPE on q and k of each token, append k, v to the cache at pos0 + t, then
+// causal attention of every query over cache positions 0 .. pos0 + t.
+hipError_t launch_attention(const void *qkv, void *kcache, void *vcache, void *q_scratch,
+                            void *out, int T, int pos0, int heads, int head_dim, float theta,
+                            hipStream_t s);
+
+}  // namespace sn

@@ -1,0 +1,627 @@
+// kernels.hip -- gfx950 (MI355X) kernels of the swap engine.
+//
+// Compute steps of a block (the per-block execution of the paper's swapping
+// cycle, Sec. 3 "Basic Idea"): implicit-GEMM convolution and token GEMM on
+// MFMA (v_mfma_f32_32x32x16_f16), a coalesced HBM-bound GEMV for batch-1
+// linear layers, pooling, bilinear upsampling, and the decoder's RMSNorm,
+// RoPE + attention and embedding gather.
+//
+// Determinism: every output's reduction order is a function of the layer
+// shape only (fixed K order, fixed MFMA instruction, fixed lane-reduction
+// tree); splitting a layer by output channels never changes any output bit.
+#include "kernels.h"
+
+#include <math.h>
+
+namespace sn {
+
+typedef _Float16 h8 __attribute__((ext_vector_type(8)));
+typedef float f16v __attribute__((ext_vector_type(16)));
+
+__device__ __forceinline__ h8 zero_h8() {
+    h8 z;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) z[i] = (_Float16)0.0f;
+    return z;
+}
+
+__device__ __forceinline__ float silu_f(float v) { return v / (1.0f + expf(-v)); }
+
+// ---------------------------------------------------------------------------
+// Implicit-GEMM convolution on MFMA.
+//
+// Block tile BM (output pixels) x BN (output channels), K tile BK.  The block
+// has WM x WN waves; each wave owns a (BM/WM) x (BN/WN) sub-tile made of
+// 32 x 32 MFMA tiles.  Operands are staged through LDS (rows padded by 16 B
+// against bank conflicts) with the next K tile prefetched into registers
+// while the current one is multiplied.
+//
+// MFMA 32x32x16 lane layout: lane l supplies A[row l%32][k (l/32)*8 .. +7]
+// and B[k ...][col l%32]; it receives C[8*(v/4) + 4*(l/32) + v%4][l%32] in
+// accumulator register v.
+// ---------------------------------------------------------------------------
+template <int BM, int BN, int BK, int WM, int WN, bool IS1X1>
+__global__ __launch_bounds__(WM *WN * 64) void conv_mfma_kernel(ConvArgs a) {
+    constexpr int NT = WM * WN * 64;
+    constexpr int LDK = BK + 8;            // halves per LDS row
+    constexpr int KC = BK / 8;             // 16-byte chunks per row
+    constexpr int A_CH = BM * KC / NT;     // A chunks per thread
+    constexpr int B_CH = BN * KC / NT;
+    constexpr int WTM = BM / WM, WTN = BN / WN;
+    constexpr int TM = WTM / 32, TN = WTN / 32;
+    static_assert(BM * KC % NT == 0 && BN * KC % NT == 0, "tile/threads mismatch");
+    static_assert(TM >= 1 && TN >= 1, "wave tile too small");
+
+    __shared__ _Float16 As[BM * LDK];
+    __shared__ _Float16 Bs[BN * LDK];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int wm = wave / WN, wn = wave % WN;
+
+    // Tile coordinates; blockIdx.x walks N tiles fastest so that consecutive
+    // blocks share the same activation rows.
+    const int n_tiles = (a.N + BN - 1) / BN;
+    const int tile_m = blockIdx.x / n_tiles;
+    const int tile_n = blockIdx.x % n_tiles;
+    const int m0 = tile_m * BM, nb0 = tile_n * BN;
+
+    const int kc = tid % KC;               // same K chunk for all of this thread's rows
+    const int row_base = tid / KC;
+    constexpr int ROW_STEP = NT / KC;
+
+    const _Float16 *xg = (const _Float16 *)a.x;
+    const _Float16 *wg = (const _Float16 *)a.w;
+
+    // Per-row input origin for the A gather.
+    int a_iy0[A_CH], a_ix0[A_CH];
+    bool a_ok[A_CH];
+#pragma unroll
+    for (int i = 0; i < A_CH; ++i) {
+        int m = m0 + row_base + i * ROW_STEP;
+        a_ok[i] = m < a.M;
+        int oy = a_ok[i] ? m / a.Wo : 0;
+        int ox = a_ok[i] ? m - oy * a.Wo : 0;
+        a_iy0[i] = oy * a.stride - a.pad;
+        a_ix0[i] = ox * a.stride - a.pad;
+    }
+
+    h8 ra[A_CH], rb[B_CH];
+    auto load_tile = [&](int k0) {
+        int k = k0 + kc * 8;
+        bool kok = k < a.K;
+        int r = 0, s = 0, ci = k;
+        if (!IS1X1 && kok) {
+            int rs = k / a.Cin_p;
+            ci = k - rs * a.Cin_p;
+            r = rs / a.kw;
+            s = rs - r * a.kw;
+        }
+#pragma unroll
+        for (int i = 0; i < A_CH; ++i) {
+            int iy = a_iy0[i] + r * a.dil;
+            int ix = a_ix0[i] + s * a.dil;
+            bool ok = kok && a_ok[i] && (IS1X1 || (iy >= 0 && iy < a.H && ix >= 0 && ix < a.W));
+            ra[i] = ok ? *(const h8 *)(xg + ((long)iy * a.W + ix) * a.Cin_p + ci) : zero_h8();
+        }
+#pragma unroll
+        for (int i = 0; i < B_CH; ++i) {
+            int n = nb0 + row_base + i * ROW_STEP;
+            bool ok = kok && n < a.N;
+            rb[i] = ok ? *(const h8 *)(wg + (long)n * a.K + k) : zero_h8();
+        }
+    };
+    auto store_tile = [&]() {
+#pragma unroll
+        for (int i = 0; i < A_CH; ++i)
+            *(h8 *)(As + (row_base + i * ROW_STEP) * LDK + kc * 8) = ra[i];
+#pragma unroll
+        for (int i = 0; i < B_CH; ++i)
+            *(h8 *)(Bs + (row_base + i * ROW_STEP) * LDK + kc * 8) = rb[i];
+    };
+
+    f16v acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
+
+    const int lrow = lane & 31;
+    const int lk = (lane >> 5) * 8;
+
+    load_tile(0);
+    for (int k0 = 0; k0 < a.K; k0 += BK) {
+        __syncthreads();
+        store_tile();
+        __syncthreads();
+        if (k0 + BK < a.K) load_tile(k0 + BK);
+#pragma unroll
+        for (int kk = 0; kk < BK; kk += 16) {
+            h8 fa[TM], fb[TN];
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+                fa[i] = *(const h8 *)(As + (wm * WTM + i * 32 + lrow) * LDK + kk + lk);
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+                fb[j] = *(const h8 *)(Bs + (wn * WTN + j * 32 + lrow) * LDK + kk + lk);
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fa[i], fb[j], acc[i][j],
+                                                                        0, 0, 0);
+        }
+    }
+
+    // Epilogue: bias, residual, ReLU / SwiGLU, one rounding to fp16.
+    _Float16 *yg = (_Float16 *)a.y;
+    const _Float16 *bg = (const _Float16 *)a.bias;
+    const _Float16 *rg = (const _Float16 *)a.res;
+    const int units = a.swiglu ? a.N / 2 : a.N;
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+            const int n = nb0 + wn * WTN + j * 32 + lrow;  // weight row (piece-local)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int m = m0 + wm * WTM + i * 32 + (v >> 2) * 8 + (lane >> 5) * 4 + (v & 3);
+                float val = acc[i][j][v];
+                if (a.swiglu) {
+                    // gate (even row) and up (odd row) sit in adjacent lanes
+                    float up = __shfl_xor(val, 1);
+                    if ((n & 1) == 0 && m < a.M && n < a.N) {
+                        float o = silu_f(val) * up;
+                        const long idx = (long)m * a.ldy + a.n0 + (n >> 1);
+                        if (rg) o += (float)rg[idx];
+                        yg[idx] = (_Float16)o;
+                    }
+                    continue;
+                }
+                if (m >= a.M) continue;
+                const long idx = (long)m * a.ldy + a.n0 + n;
+                if (n < a.N) {
+                    if (bg) val += (float)bg[n];
+                    if (rg) val += (float)rg[idx];
+                    if (a.relu) val = fmaxf(val, 0.0f);
+                    yg[idx] = (_Float16)val;
+                } else if (a.n0 + n < a.n_zero_end) {
+                    yg[idx] = (_Float16)0.0f;
+                }
+            }
+        }
+    }
+    (void)units;
+}
+
+struct ConvVariant {
+    int bm, bn, bk;
+    bool is1x1;
+    const char *name;
+    void (*fn)(ConvArgs);
+    int threads;
+};
+
+#define SN_CONV_VARIANT(BM, BN, BK, WM, WN, ONE, SUFFIX)                          \
+    {BM, BN, BK, ONE, "conv_mfma_" #BM "x" #BN "x" #BK "_w" #WM #WN SUFFIX, \
+     conv_mfma_kernel<BM, BN, BK, WM, WN, ONE>, WM * WN * 64}
+#define SN_CONV_PAIR(BM, BN, BK, WM, WN) \
+    SN_CONV_VARIANT(BM, BN, BK, WM, WN, false, "_gen"), SN_CONV_VARIANT(BM, BN, BK, WM, WN, true, "_1x1")
+
+static const ConvVariant kConvVariants[] = {
+    SN_CONV_PAIR(128, 128, 32, 2, 2), SN_CONV_PAIR(128, 64, 32, 2, 2),
+    SN_CONV_PAIR(64, 128, 32, 2, 2),  SN_CONV_PAIR(64, 64, 32, 2, 2),
+    SN_CONV_PAIR(32, 64, 64, 1, 2),   SN_CONV_PAIR(32, 32, 64, 1, 1),
+};
+static constexpr int kNumConvVariants = sizeof(kConvVariants) / sizeof(kConvVariants[0]);
+
+int conv_kernel_count() { return kNumConvVariants; }
+const char *conv_kernel_name(int id) {
+    return (id >= 0 && id < kNumConvVariants) ? kConvVariants[id].name : "?";
+}
+
+// Tile choice from the full layer shape (never from a slab's channel range):
+// the largest tile that still gives every CU a block, else the one with most
+// blocks.
+int conv_kernel_choice(int M, int N, int K, bool is1x1) {
+    const int cus = 256;
+    int best = -1;
+    long best_blocks = -1;
+    for (int id = 0; id < kNumConvVariants; ++id) {
+        const ConvVariant &v = kConvVariants[id];
+        if (v.is1x1 != is1x1) continue;
+        long blocks = (long)((M + v.bm - 1) / v.bm) * ((N + v.bn - 1) / v.bn);
+        if (blocks >= cus) return id;
+        if (blocks > best_blocks) {
+            best_blocks = blocks;
+            best = id;
+        }
+    }
+    (void)K;
+    return best;
+}
+
+hipError_t launch_conv(int kernel, const ConvArgs &a, hipStream_t s) {
+    if (kernel < 0 || kernel >= kNumConvVariants) return hipErrorInvalidValue;
+    const ConvVariant &v = kConvVariants[kernel];
+    if (a.M <= 0 || a.N <= 0) return hipSuccess;
+    long blocks = (long)((a.M + v.bm - 1) / v.bm) * ((a.N + v.bn - 1) / v.bn);
+    hipLaunchKernelGGL(v.fn, dim3((unsigned)blocks), dim3(v.threads), 0, s, a);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// GEMV (batch-1 linear).  The input vector is staged in LDS once per block;
+// each wave streams ROWS weight rows with 16-byte loads, four chunks in
+// flight per row, accumulating in fp32 in a fixed order, then reduces across
+// the 64 lanes with a fixed butterfly.
+// ---------------------------------------------------------------------------
+template <int ROWS>
+__global__ __launch_bounds__(256) void gemv_kernel(GemvArgs a) {
+    extern __shared__ h8 xs[];
+    const int tid = threadIdx.x;
+    const int kch = a.K / 8;
+    if (blockIdx.x == 0 && a.zero_end > 0) {
+        const int first = a.n0 + (a.swiglu ? a.rows / 2 : a.rows);
+        for (int n = first + tid; n < a.zero_end; n += 256) {
+            if (a.out_f32) ((float *)a.y)[n] = 0.0f;
+            else ((_Float16 *)a.y)[n] = (_Float16)0.0f;
+        }
+    }
+    const h8 *xg = (const h8 *)a.x;
+    for (int c = tid; c < kch; c += 256) xs[c] = xg[c];
+    __syncthreads();
+
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int row0 = (blockIdx.x * 4 + wave) * ROWS;
+    if (row0 >= a.rows) return;
+    const h8 *wg = (const h8 *)a.w;
+
+    float acc[ROWS];
+#pragma unroll
+    for (int r = 0; r < ROWS; ++r) acc[r] = 0.0f;
+
+    int c = lane;
+    for (; c + 192 < kch; c += 256) {
+        h8 xv0 = xs[c], xv1 = xs[c + 64], xv2 = xs[c + 128], xv3 = xs[c + 192];
+#pragma unroll
+        for (int r = 0; r < ROWS; ++r) {
+            if (row0 + r < a.rows) {
+                const h8 *wr = wg + (long)(row0 + r) * kch;
+                h8 w0 = wr[c], w1 = wr[c + 64], w2 = wr[c + 128], w3 = wr[c + 192];
+                float s = acc[r];
+#pragma unroll
+                for (int i = 0; i < 8; ++i) s = fmaf((float)w0[i], (float)xv0[i], s);
+#pragma unroll
+                for (int i = 0; i < 8; ++i) s = fmaf((float)w1[i], (float)xv1[i], s);
+#pragma unroll
+                for (int i = 0; i < 8; ++i) s = fmaf((float)w2[i], (float)xv2[i], s);
+#pragma unroll
+                for (int i = 0; i < 8; ++i) s = fmaf((float)w3[i], (float)xv3[i], s);
+                acc[r] = s;
+            }
+        }
+    }
+    for (; c < kch; c += 64) {
+        h8 xv = xs[c];
+#pragma unroll
+        for (int r = 0; r < ROWS; ++r) {
+            if (row0 + r < a.rows) {
+                h8 wv = wg[(long)(row0 + r) * kch + c];
+                float s = acc[r];
+#pragma unroll
+                for (int i = 0; i < 8; ++i) s = fmaf((float)wv[i], (float)xv[i], s);
+                acc[r] = s;
+            }
+        }
+    }
+#pragma unroll
+    for (int r = 0; r < ROWS; ++r) {
+        float v = acc[r];
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
+        acc[r] = v;
+    }
+    if (lane != 0) return;
+    const _Float16 *bg = (const _Float16 *)a.bias;
+    const _Float16 *rg = (const _Float16 *)a.res;
+    if (a.swiglu) {
+#pragma unroll
+        for (int r = 0; r + 1 < ROWS; r += 2) {
+            int row = row0 + r;
+            if (row + 1 >= a.rows) break;
+            int n = a.n0 + (row >> 1);
+            float o = silu_f(acc[r]) * acc[r + 1];
+            if (rg) o += (float)rg[n];
+            if (a.out_f32) ((float *)a.y)[n] = o;
+            else ((_Float16 *)a.y)[n] = (_Float16)o;
+        }
+        return;
+    }
+#pragma unroll
+    for (int r = 0; r < ROWS; ++r) {
+        int row = row0 + r;
+        if (row >= a.rows) break;
+        int n = a.n0 + row;
+        float o = acc[r];
+        if (bg) o += (float)bg[row];
+        if (rg) o += (float)rg[n];
+        if (a.relu) o = fmaxf(o, 0.0f);
+        if (a.out_f32) ((float *)a.y)[n] = o;
+        else ((_Float16 *)a.y)[n] = (_Float16)o;
+    }
+}
+
+hipError_t launch_gemv(const GemvArgs &a, hipStream_t s) {
+    if (a.rows <= 0) return hipSuccess;
+    if (a.K % 8) return hipErrorInvalidValue;
+    constexpr int ROWS = 2;   // even, so SwiGLU pairs stay in one wave
+    unsigned blocks = (unsigned)((a.rows + 4 * ROWS - 1) / (4 * ROWS));
+    size_t lds = (size_t)a.K * 2;
+    hipLaunchKernelGGL(gemv_kernel<ROWS>, dim3(blocks), dim3(256), lds, s, a);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Pooling, upsampling and layout conversion (memory-bound, 8 channels per
+// thread with 16-byte accesses).
+// ---------------------------------------------------------------------------
+__global__ void maxpool_kernel(const _Float16 *x, _Float16 *y, int H, int W, int Cp, int Ho,
+                               int Wo, int k, int stride, int pad) {
+    const int cg = Cp / 8;
+    long t = (long)blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= (long)Ho * Wo * cg) return;
+    int c8 = (int)(t % cg);
+    long p = t / cg;
+    int ox = (int)(p % Wo), oy = (int)(p / Wo);
+    float m[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) m[i] = -INFINITY;
+    for (int r = 0; r < k; ++r) {
+        int iy = oy * stride - pad + r;
+        if (iy < 0 || iy >= H) continue;
+        for (int s = 0; s < k; ++s) {
+            int ix = ox * stride - pad + s;
+            if (ix < 0 || ix >= W) continue;
+            h8 v = *(const h8 *)(x + ((long)iy * W + ix) * Cp + c8 * 8);
+#pragma unroll
+            for (int i = 0; i < 8; ++i) m[i] = fmaxf(m[i], (float)v[i]);
+        }
+    }
+    h8 o;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) o[i] = (_Float16)m[i];
+    *(h8 *)(y + p * Cp + c8 * 8) = o;
+}
+
+hipError_t launch_maxpool(const void *x, void *y, int H, int W, int Cp, int Ho, int Wo, int k,
+                          int stride, int pad, hipStream_t s) {
+    long n = (long)Ho * Wo * (Cp / 8);
+    hipLaunchKernelGGL(maxpool_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s,
+                       (const _Float16 *)x, (_Float16 *)y, H, W, Cp, Ho, Wo, k, stride, pad);
+    return hipGetLastError();
+}
+
+// Mean over H*W per channel: one thread per channel, pixels summed in order.
+__global__ void gavgpool_kernel(const _Float16 *x, _Float16 *y, int HW, int Cp) {
+    int c = blockIdx.x * blockDim.x + threadIdx.x;
+    if (c >= Cp) return;
+    float s = 0.0f;
+    for (int p = 0; p < HW; ++p) s += (float)x[(long)p * Cp + c];
+    y[c] = (_Float16)(s / (float)HW);
+}
+
+hipError_t launch_gavgpool(const void *x, void *y, int HW, int Cp, hipStream_t s) {
+    hipLaunchKernelGGL(gavgpool_kernel, dim3((Cp + 63) / 64), dim3(64), 0, s, (const _Float16 *)x,
+                       (_Float16 *)y, HW, Cp);
+    return hipGetLastError();
+}
+
+// Bilinear, integer factor, half-pixel centres: source = (o + 0.5)/scale - 0.5
+// clamped at 0, upper neighbour clamped to the edge.
+__global__ void upsample_kernel(const _Float16 *x, _Float16 *y, int H, int W, int Cp, int scale) {
+    const int cg = Cp / 8;
+    const int Ho = H * scale, Wo = W * scale;
+    long t = (long)blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= (long)Ho * Wo * cg) return;
+    int c8 = (int)(t % cg);
+    long p = t / cg;
+    int ox = (int)(p % Wo), oy = (int)(p / Wo);
+    float inv = 1.0f / (float)scale;
+    float sy = fmaxf(((float)oy + 0.5f) * inv - 0.5f, 0.0f);
+    float sx = fmaxf(((float)ox + 0.5f) * inv - 0.5f, 0.0f);
+    int y0 = min((int)sy, H - 1), x0 = min((int)sx, W - 1);
+    int y1 = min(y0 + 1, H - 1), x1 = min(x0 + 1, W - 1);
+    float ly = sy - (float)y0, lx = sx - (float)x0;
+    h8 a = *(const h8 *)(x + ((long)y0 * W + x0) * Cp + c8 * 8);
+    h8 b = *(const h8 *)(x + ((long)y0 * W + x1) * Cp + c8 * 8);
+    h8 c = *(const h8 *)(x + ((long)y1 * W + x0) * Cp + c8 * 8);
+    h8 d = *(const h8 *)(x + ((long)y1 * W + x1) * Cp + c8 * 8);
+    h8 o;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        float top = (float)a[i] * (1.0f - lx) + (float)b[i] * lx;
+        float bot = (float)c[i] * (1.0f - lx) + (float)d[i] * lx;
+        o[i] = (_Float16)(top * (1.0f - ly) + bot * ly);
+    }
+    *(h8 *)(y + p * Cp + c8 * 8) = o;
+}
+
+hipError_t launch_upsample(const void *x, void *y, int H, int W, int Cp, int scale, hipStream_t s) {
+    long n = (long)H * scale * W * scale * (Cp / 8);
+    hipLaunchKernelGGL(upsample_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s,
+                       (const _Float16 *)x, (_Float16 *)y, H, W, Cp, scale);
+    return hipGetLastError();
+}
+
+__global__ void chw_to_hwc_kernel(const _Float16 *x, _Float16 *y, int C, int HW, int Cp) {
+    long t = (long)blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= (long)HW * Cp) return;
+    int c = (int)(t % Cp);
+    long p = t / Cp;
+    y[t] = c < C ? x[(long)c * HW + p] : (_Float16)0.0f;
+}
+
+hipError_t launch_chw_to_hwc(const void *x, void *y, int C, int H, int W, int Cp, hipStream_t s) {
+    long n = (long)H * W * Cp;
+    hipLaunchKernelGGL(chw_to_hwc_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s,
+                       (const _Float16 *)x, (_Float16 *)y, C, H * W, Cp);
+    return hipGetLastError();
+}
+
+__global__ void hwc_to_chw_kernel(const _Float16 *x, _Float16 *y, int C, int HW, int Cp) {
+    long t = (long)blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= (long)HW * C) return;
+    long p = t % HW;
+    int c = (int)(t / HW);
+    y[t] = x[p * Cp + c];
+}
+
+hipError_t launch_hwc_to_chw(const void *x, void *y, int C, int H, int W, int Cp, hipStream_t s) {
+    long n = (long)H * W * C;
+    hipLaunchKernelGGL(hwc_to_chw_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s,
+                       (const _Float16 *)x, (_Float16 *)y, C, H * W, Cp);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Decoder kernels.
+// ---------------------------------------------------------------------------
+
+// Embedding rows gathered straight from the pinned host table (mapped into
+// the device address space): only the rows of the given ids cross the link.
+__global__ void embed_kernel(const int32_t *ids, const _Float16 *table, _Float16 *y, int d) {
+    int t = blockIdx.x;
+    long row = ids[t];
+    const h8 *src = (const h8 *)(table + row * d);
+    h8 *dst = (h8 *)(y + (long)t * d);
+    for (int c = threadIdx.x; c < d / 8; c += blockDim.x) dst[c] = src[c];
+}
+
+hipError_t launch_embed(const int32_t *ids, const void *table, void *y, int T, int d, hipStream_t s) {
+    hipLaunchKernelGGL(embed_kernel, dim3(T), dim3(256), 0, s, ids, (const _Float16 *)table,
+                       (_Float16 *)y, d);
+    return hipGetLastError();
+}
+
+// Block-wide fixed-order sum (256 threads).
+__device__ float block_sum_256(float v, float *red) {
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
+    const int wave = threadIdx.x >> 6;
+    __syncthreads();
+    if ((threadIdx.x & 63) == 0) red[wave] = v;
+    __syncthreads();
+    return (red[0] + red[1]) + (red[2] + red[3]);
+}
+
+__global__ __launch_bounds__(256) void rmsnorm_kernel(const _Float16 *x, const _Float16 *g,
+                                                      _Float16 *y, int d, float eps) {
+    __shared__ float red[4];
+    const _Float16 *xr = x + (long)blockIdx.x * d;
+    float s = 0.0f;
+    for (int c = threadIdx.x; c < d; c += 256) {
+        float v = (float)xr[c];
+        s = fmaf(v, v, s);
+    }
+    s = block_sum_256(s, red);
+    float scale = 1.0f / sqrtf(s / (float)d + eps);
+    _Float16 *yr = y + (long)blockIdx.x * d;
+    for (int c = threadIdx.x; c < d; c += 256) yr[c] = (_Float16)((float)xr[c] * scale * (float)g[c]);
+}
+
+hipError_t launch_rmsnorm(const void *x, const void *gain, void *y, int T, int d, float eps,
+                          hipStream_t s) {
+    hipLaunchKernelGGL(rmsnorm_kernel, dim3(T), dim3(256), 0, s, (const _Float16 *)x,
+                       (const _Float16 *)gain, (_Float16 *)y, d, eps);
+    return hipGetLastError();
+}
+
+// RoPE (rotate-half) on q and k; q goes to q_scratch (fp32), k and v to the
+// cache at position pos0 + t.  One block per token, one thread per pair.
+__global__ void rope_append_kernel(const _Float16 *qkv, float *qs, _Float16 *kc, _Float16 *vc,
+                                   int pos0, int heads, int hd, float theta) {
+    const int t = blockIdx.x;
+    const int d = heads * hd;
+    const int half = hd / 2;
+    const _Float16 *row = qkv + (long)t * 3 * d;
+    const long pos = pos0 + t;
+    for (int p = threadIdx.x; p < heads * half; p += blockDim.x) {
+        int h = p / half, i = p - (p / half) * half;
+        double ang = (double)pos * pow((double)theta, -2.0 * (double)i / (double)hd);
+        float cs = (float)cos(ang), sn = (float)sin(ang);
+        int a = h * hd + i, b = a + half;
+        float qa = (float)row[a], qb = (float)row[b];
+        qs[(long)t * d + a] = qa * cs - qb * sn;
+        qs[(long)t * d + b] = qb * cs + qa * sn;
+        float ka = (float)row[d + a], kb = (float)row[d + b];
+        kc[pos * d + a] = (_Float16)(ka * cs - kb * sn);
+        kc[pos * d + b] = (_Float16)(kb * cs + ka * sn);
+        vc[pos * d + a] = row[2 * d + a];
+        vc[pos * d + b] = row[2 * d + b];
+    }
+}
+
+// One block per (token, head): scores over cache positions 0..pos0+t in LDS,
+// fixed-order max / sum reductions, then each thread owns one output dim and
+// accumulates over positions in order.
+__global__ __launch_bounds__(256) void attention_kernel(const float *qs, const _Float16 *kc,
+                                                        const _Float16 *vc, _Float16 *out,
+                                                        int pos0, int heads, int hd) {
+    extern __shared__ float sc[];
+    __shared__ float red[4];
+    const int t = blockIdx.x / heads, h = blockIdx.x % heads;
+    const int d = heads * hd;
+    const int nk = pos0 + t + 1;
+    const float *q = qs + (long)t * d + h * hd;
+    const float scale = 1.0f / sqrtf((float)hd);
+    for (int j = threadIdx.x; j < nk; j += 256) {
+        const _Float16 *kr = kc + (long)j * d + h * hd;
+        float s = 0.0f;
+        for (int i = 0; i < hd; ++i) s = fmaf(q[i], (float)kr[i], s);
+        sc[j] = s * scale;
+    }
+    __syncthreads();
+    float m = -INFINITY;
+    for (int j = threadIdx.x; j < nk; j += 256) m = fmaxf(m, sc[j]);
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
+    __syncthreads();
+    m = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+    __syncthreads();
+    float sum = 0.0f;
+    for (int j = threadIdx.x; j < nk; j += 256) {
+        float e = expf(sc[j] - m);
+        sc[j] = e;
+        sum += e;
+    }
+    sum = block_sum_256(sum, red);
+    const float inv = 1.0f / sum;
+    for (int i = threadIdx.x; i < hd; i += 256) {
+        float o = 0.0f;
+        for (int j = 0; j < nk; ++j) o = fmaf(sc[j], (float)vc[(long)j * d + h * hd + i], o);
+        out[(long)t * d + h * hd + i] = (_Float16)(o * inv);
+    }
+}
+
+hipError_t launch_attention(const void *qkv, void *kcache, void *vcache, void *q_scratch,
+                            void *out, int T, int pos0, int heads, int head_dim, float theta,
+                            hipStream_t s) {
+    hipLaunchKernelGGL(rope_append_kernel, dim3(T), dim3(256), 0, s, (const _Float16 *)qkv,
+                       (float *)q_scratch, (_Float16 *)kcache, (_Float16 *)vcache, pos0, heads,
+                       head_dim, theta);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    size_t lds = (size_t)(pos0 + T) * sizeof(float);
+    hipLaunchKernelGGL(attention_kernel, dim3(T * heads), dim3(256), lds, s,
+                       (const float *)q_scratch, (const _Float16 *)kcache,
+                       (const _Float16 *)vcache, (_Float16 *)out, pos0, heads, head_dim);
+    return hipGetLastError();
+}
+
+}  // namespace sn

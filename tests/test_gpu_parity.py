@@ -1,0 +1,203 @@
+"""GPU parity: the HIP engine (through the C ABI) against the fp64 oracle.
+
+Bar: max|gpu - ref| <= 1e-2 * max|ref| on the final output of each network
+(per step for the decoder); swapped runs bit-identical to all-resident runs
+and to runs with a different slab partition.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2401_16757_amd import swapnet as S
+from paper_2401_16757_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-2
+
+
+def rel_err(got, ref):
+    ref = np.asarray(ref, np.float64)
+    return float(np.abs(np.asarray(got, np.float64) - ref).max() / np.abs(ref).max())
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    S.load_library()
+
+
+_cache = {}
+
+
+def net_case(name, **kw):
+    key = (name, tuple(sorted(kw.items())))
+    if key not in _cache:
+        net = W.get_network(name, **kw)
+        wts = W.make_weights(net)
+        x = W.make_input(net)
+        ref = oracle.forward(net, wts, x)
+        _cache[key] = (net, wts, x, ref)
+    return _cache[key]
+
+
+def run(net, wts, x, **kw):
+    with S.build_engine(net, wts, **kw) as eng:
+        st = eng.stats()
+        y = eng.infer(x)
+        y2 = eng.infer(x)
+    assert np.array_equal(y.view(np.uint16), y2.view(np.uint16)), "repeat run not bit-identical"
+    return y, st
+
+
+CNN_CASES = [("tiny_cnn", {}), ("resnet50", {}), ("vgg16", {}), ("fcn_resnet101", {}),
+             ("resnet50", {"res": 96}), ("fcn_resnet101", {"res": 128}), ("vgg16", {"res": 64})]
+
+
+@pytest.mark.parametrize("name,kw", CNN_CASES)
+def test_swapped_matches_oracle_and_resident(name, kw):
+    print(f"[case] {name} {kw}", flush=True)
+    net, wts, x, ref = net_case(name, **kw)
+    budget = net.budget_bytes()
+    y, st = run(net, wts, x, budget=budget)
+    assert st["resident"] == 0 and st["n_slabs"] >= 2
+    assert st["arena_high_water"] <= budget
+    err = rel_err(y, ref)
+    print(f"  swapped slabs={st['n_slabs']} err={err:.2e}", flush=True)
+    assert err <= TOL
+    big = st["image_bytes"] + 4096
+    # all-resident with the same slabs, all-resident unsplit, and a stricter partition
+    y_res_same, st1 = run(net, wts, x, budget=big, split_budget=budget)
+    y_res, st2 = run(net, wts, x, budget=big)
+    assert st1["resident"] == 1 and st2["resident"] == 1
+    for other in (y_res_same, y_res):
+        assert np.array_equal(y.view(np.uint16), other.view(np.uint16))
+    tight = max(int(net.weight_bytes() / 5.81), 4 * 1024)
+    try:
+        y_tight, st3 = run(net, wts, x, budget=tight)
+    except S.SwapNetError as e:
+        assert e.code == S.SN_E_INFEASIBLE
+    else:
+        assert st3["n_slabs"] >= st["n_slabs"]
+        assert np.array_equal(y.view(np.uint16), y_tight.view(np.uint16))
+
+
+def single_layer_net(spec, cfg=90):
+    spec.src, spec.dst = 0, 1
+    net = W.Network("one_" + spec.op, cfg, [spec], [[0, 1]], (spec.c_in, spec.h_in, spec.w_in), 1)
+    return net
+
+
+CONV_SHAPES = [
+    # c_in, c_out, h, w, k, stride, pad, dil
+    (3, 16, 32, 32, 3, 1, 1, 1), (3, 64, 37, 29, 7, 2, 3, 1), (16, 40, 17, 19, 3, 2, 1, 1),
+    (64, 72, 9, 11, 3, 1, 2, 2), (32, 24, 13, 13, 3, 1, 4, 4), (256, 520, 7, 7, 1, 1, 0, 1),
+    (24, 200, 15, 15, 1, 2, 0, 1), (512, 96, 7, 7, 3, 1, 1, 1), (8, 21, 40, 40, 1, 1, 0, 1),
+    (128, 256, 56, 56, 1, 1, 0, 1), (64, 64, 56, 56, 3, 1, 1, 1),
+]
+
+
+@pytest.mark.parametrize("shape", CONV_SHAPES)
+def test_conv_kernel_parity_and_slice_invariance(shape):
+    ci, co, h, w, k, st, pad, dil = shape
+    print(f"[case] conv {shape}", flush=True)
+    spec = W.LayerSpec(name="c", op="conv2d", src=0, dst=1, c_in=ci, c_out=co, h_in=h, w_in=w,
+                       k=k, stride=st, pad=pad, dilation=dil, relu=True, bn=True)
+    net = single_layer_net(spec)
+    wts = W.make_weights(net)
+    x = W.make_input(net)
+    ref = oracle.forward(net, wts, x)
+    y, _ = run(net, wts, x, budget=1 << 30)
+    assert rel_err(y, ref) <= TOL
+    # split the layer by output channels: every output bit must be unchanged
+    wbytes = net.weight_bytes()
+    for parts in (2, 3, 5):
+        y2, st2 = run(net, wts, x, budget=1 << 30, split_budget=max(2 * wbytes // parts, 2048))
+        assert st2["n_slabs"] >= 2
+        assert np.array_equal(y.view(np.uint16), y2.view(np.uint16)), parts
+
+
+LINEAR_SHAPES = [(64, 10, False), (2048, 1000, True), (25088, 4096, True), (4096, 37, False),
+                 (520, 1003, True)]
+
+
+@pytest.mark.parametrize("k_in,n_out,relu", LINEAR_SHAPES)
+def test_linear_kernel_parity_and_slice_invariance(k_in, n_out, relu):
+    print(f"[case] linear {k_in}->{n_out}", flush=True)
+    spec = W.LayerSpec(name="fc", op="linear", src=0, dst=1, c_in=k_in, c_out=n_out, relu=relu)
+    net = W.Network("one_linear", 91, [spec], [[0, 1]], (k_in, 1, 1), 1)
+    wts = W.make_weights(net)
+    x = W.make_input(net)
+    ref = oracle.forward(net, wts, x)
+    y, _ = run(net, wts, x, budget=1 << 30)
+    assert rel_err(y, ref) <= TOL
+    y2, st2 = run(net, wts, x, budget=1 << 30, split_budget=max(net.weight_bytes() // 2, 4096))
+    assert st2["n_slabs"] >= 2
+    assert np.array_equal(y.view(np.uint16), y2.view(np.uint16))
+
+
+def test_infer_dev_on_torch_stream_matches_host_path():
+    net, wts, x, ref = net_case("resnet50", res=96)
+    with S.build_engine(net, wts) as eng:
+        y_host = eng.infer(x)
+        xd = torch.from_numpy(x).cuda()
+        yd = torch.empty(eng.out_shape, dtype=torch.float16, device="cuda")
+        s = torch.cuda.Stream()
+        with torch.cuda.stream(s):
+            for _ in range(3):
+                eng.infer_dev(xd.data_ptr(), yd.data_ptr(), s.cuda_stream)
+        s.synchronize()
+        assert np.array_equal(yd.cpu().numpy().view(np.uint16), y_host.view(np.uint16))
+
+
+def small_decoder(**kw):
+    a = dict(n_layers=2, d=128, heads=4, ffn=160, vocab=300, max_seq=48, prompt=24, gen=8)
+    a.update(kw)
+    return W.decoder7b(**a)
+
+
+def test_decoder_teacher_forced_parity():
+    net = small_decoder()
+    wts = W.make_weights(net)
+    prompt = W.make_input(net)
+    gen = net.extra["gen"]
+    lb = sum(l.weight_bytes() for l in net.layers[1:8])
+    for budget, split in ((2 * lb, None), (1 << 30, 2 * lb)):
+        eng = S.build_engine(net, wts, budget=budget, split_budget=split)
+        rows, fed = [], []
+        logits = eng.infer_tokens(prompt)
+        rows.append(logits)
+        for _ in range(gen - 1):
+            nxt = int(np.argmax(logits))
+            fed.append(nxt)
+            logits = eng.infer_tokens(np.array([nxt], np.int32))
+            rows.append(logits)
+        eng.close()
+        seq = np.concatenate([prompt, np.array(fed, np.int32)])
+        ref = oracle.decoder_forward(net, wts, seq)
+        got = np.stack(rows)
+        want = ref[len(prompt) - 1:]
+        for t in range(gen):
+            assert rel_err(got[t], want[t]) <= TOL, t
+        if split is None:
+            first = got
+        else:
+            assert np.array_equal(first.view(np.uint32), got.view(np.uint32))
+
+
+def test_decoder_prefill_uses_mfma_path_and_decode_matches_prefix():
+    """Logits of a prompt processed in one call equal (to the bar) the logits
+    of the same tokens fed one by one (GEMM path vs GEMV path)."""
+    net = small_decoder()
+    wts = W.make_weights(net)
+    prompt = W.make_input(net)[:10]
+    with S.build_engine(net, wts, budget=1 << 30) as eng:
+        a = eng.infer_tokens(prompt)
+        eng.reset()
+        for t in prompt:
+            b = eng.infer_tokens(np.array([t], np.int32))
+    ref = oracle.decoder_forward(net, wts, prompt)[-1]
+    assert rel_err(a, ref) <= TOL
+    assert rel_err(b, ref) <= TOL
