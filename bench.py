@@ -1,0 +1,324 @@
+"""Benchmark of block-swapped inference on one MI355X.
+
+One step = one inference of the whole hot path over one input: every slab
+streamed from the pinned host image into the budgeted HBM arena (one DMA per
+slab, copy stream), bound by pointer, computed by the HIP kernels on the
+compute stream, its range reused by the slab two places later.  The network
+input is resident in HBM when the timed region starts; the weights are in
+pinned host memory, as the method intends.
+
+Prints ONE JSON line with
+  value     swapped / all-resident latency ratio (lower is better);
+  h2d_*     streamed weight bytes per second vs the measured pinned-H2D peak;
+  roofline  the dominant compute kernel against the MFMA fp16 peak;
+  link      the swap DMA against the measured pinned-H2D peak;
+  cpu_baseline  the fp64 CPU oracle on this host (a baseline, not a target).
+
+Usage: python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--workload resnet50]
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+MFMA_FP16_PEAK_TFLOPS = 2500.0     # MI355X dense fp16 MFMA
+HBM_PEAK_GBS = 8000.0
+METRIC = "swapped/all-resident latency ratio at budget; H2D GB/s vs link peak; MFMA util"
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="resnet50",
+                    choices=["tiny_cnn", "resnet50", "vgg16", "fcn_resnet101"])
+    ap.add_argument("--budget-frac", type=float, default=None,
+                    help="budget as a fraction of the weight bytes (default: the workload's)")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="approximate CPU time spent on the oracle baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--verbose", action="store_true")
+    ap.add_argument("--no-graph", action="store_true", help="enqueue call by call (no HIP graph)")
+    return ap.parse_args()
+
+
+def log(msg):
+    print("[bench] " + msg, file=sys.stderr, flush=True)
+
+
+def measure_h2d_peak(torch, sizes=(64 << 20, 256 << 20), reps=8):
+    """Best sustained pinned host -> device copy rate (GB/s) over large copies,
+    using the same runtime call as the engine (hipMemcpyAsync via torch)."""
+    best = 0.0
+    n_max = max(sizes)
+    h = torch.empty(n_max, dtype=torch.uint8, pin_memory=True)
+    h.fill_(1)
+    d = torch.empty(n_max, dtype=torch.uint8, device="cuda")
+    s = torch.cuda.current_stream()
+    for n in sizes:
+        for _ in range(2):
+            d[:n].copy_(h[:n], non_blocking=True)
+        torch.cuda.synchronize()
+        rates = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(s)
+            d[:n].copy_(h[:n], non_blocking=True)
+            e1.record(s)
+            e1.synchronize()
+            rates.append(n / (e0.elapsed_time(e1) * 1e-3) / 1e9)
+        best = max(best, float(np.median(rates)))
+    del h, d
+    return best
+
+
+def timed_loop(torch, eng, xd, yd, steps, warmup):
+    s = torch.cuda.current_stream()
+    for _ in range(warmup):
+        eng.infer_dev(xd.data_ptr(), yd.data_ptr(), s.cuda_stream)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record(s)
+    for _ in range(steps):
+        eng.infer_dev(xd.data_ptr(), yd.data_ptr(), s.cuda_stream)
+    e1.record(s)
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) * 1e3
+    return e0.elapsed_time(e1) / steps, wall / steps
+
+
+def host_enqueue_us(torch, eng, xd, yd, n=10):
+    """Host time of one sn_infer_dev call (the enqueue only), GPU idle."""
+    s = torch.cuda.current_stream()
+    ts = []
+    for _ in range(n):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        eng.infer_dev(xd.data_ptr(), yd.data_ptr(), s.cuda_stream)
+        ts.append((time.perf_counter() - t0) * 1e6)
+    torch.cuda.synchronize()
+    return float(np.median(ts))
+
+
+def single_latency(torch, eng, xd, yd, n=10):
+    """Latency of one isolated inference (no overlap with the previous one)."""
+    s = torch.cuda.current_stream()
+    ts = []
+    for _ in range(n):
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(s)
+        eng.infer_dev(xd.data_ptr(), yd.data_ptr(), s.cuda_stream)
+        e1.record(s)
+        e1.synchronize()
+        ts.append(e0.elapsed_time(e1))
+    return float(np.median(ts))
+
+
+def conv_flops(spec, c0, c1):
+    ho, wo = spec.out_hw()
+    return 2.0 * ho * wo * (c1 - c0) * spec.c_in * spec.k * spec.k
+
+
+def kernel_profile(S, net, eng, torch, xd, yd):
+    """Per-piece kernel times of one inference (timing level 2), grouped by
+    kernel.  Returns {name: (launches, total_ms, flops, bytes)}."""
+    s = torch.cuda.current_stream()
+    eng.set_option(S.OPT_TIMING, 2)
+    for _ in range(2):
+        eng.infer_dev(xd.data_ptr(), yd.data_ptr(), s.cuda_stream)
+        torch.cuda.synchronize()
+    # the per-piece events are read back by a host-API call
+    x = xd.cpu().numpy()
+    eng.infer(x)
+    eng.set_option(S.OPT_TIMING, 0)
+    groups = {}
+    for p in eng.pieces():
+        spec = net.layers[p["layer"]]
+        if spec.op == "conv2d":
+            name = S.kernel_name(p["kernel"])
+            fl = conv_flops(spec, p["c0"], p["c1"])
+            by = p["w_bytes"] + p["b_bytes"]
+        elif spec.op == "linear":
+            name = "gemv"
+            fl = 2.0 * (p["c1"] - p["c0"]) * spec.c_in
+            by = p["w_bytes"] + p["b_bytes"] + 2 * spec.c_in + 2 * (p["c1"] - p["c0"])
+        else:
+            name = spec.op
+            fl, by = 0.0, 0.0
+        g = groups.setdefault(name, [0, 0.0, 0.0, 0.0])
+        g[0] += 1
+        g[1] += p["t_ms"]
+        g[2] += fl
+        g[3] += by
+    return groups
+
+
+def slab_timeline(S, eng, x):
+    """DMA / compute intervals of each slab in one host-API inference."""
+    eng.set_option(S.OPT_TIMING, 1)
+    eng.infer(x)
+    eng.set_option(S.OPT_TIMING, 0)
+    sl = eng.slabs()
+    dma = [(s["t_in_start_ms"], s["t_in_start_ms"] + s["t_in_ms"]) for s in sl]
+    comp = [(s["t_ex_start_ms"], s["t_ex_start_ms"] + s["t_ex_ms"]) for s in sl]
+    dma_total = sum(b - a for a, b in dma)
+    inter = 0.0
+    for a, b in dma:
+        for c, d in comp:
+            inter += max(0.0, min(b, d) - max(a, c))
+    return {"dma_ms": round(dma_total, 4), "compute_ms": round(sum(b - a for a, b in comp), 4),
+            "overlap_frac": round(inter / dma_total, 4) if dma_total > 0 else None,
+            "per_slab": [{"bytes": s["bytes"], "t_in_ms": round(s["t_in_ms"], 4),
+                          "t_ex_ms": round(s["t_ex_ms"], 4),
+                          "dma_gbs": round(s["bytes"] / (s["t_in_ms"] * 1e6), 2)
+                          if s["t_in_ms"] > 0 else None} for s in sl]}
+
+
+def cpu_baseline(net, wts, x, seconds):
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()
+                       if i.get("user_api") == "blas"] or [1])
+    except Exception:
+        threads = os.cpu_count()
+    t0 = time.perf_counter()
+    n = 0
+    while True:
+        oracle.forward(net, wts, x)
+        n += 1
+        el = time.perf_counter() - t0
+        if el >= seconds or n >= 200:
+            break
+    return {"value": round(el / n * 1e3, 3), "unit": "ms/inference", "cores": int(threads),
+            "kind": "oracle",
+            "sample": "%d fp64 forward passes of %s (%.1f s) on host BLAS threads"
+                      % (n, net.name, el)}
+
+
+def main():
+    a = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if a.gpus != 1 or world != 1:
+        print("bench.py: this engine runs on one GPU; --gpus %d is not supported "
+              "(multi-GPU sharding is a design note only)" % a.gpus, file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2401_16757_amd import swapnet as S
+    from paper_2401_16757_amd import workloads as W
+
+    torch.cuda.set_device(0)
+    # all engine work goes to a non-default stream, so that torch's events
+    # (recorded on the current stream) bracket it
+    stream = torch.cuda.Stream()
+    torch.cuda.set_stream(stream)
+    net = W.get_network(a.workload)
+    log("generating %s weights" % net.name)
+    wts = W.make_weights(net)
+    x = W.make_input(net)
+    budget = net.budget_bytes() if a.budget_frac is None else int(net.weight_bytes() * a.budget_frac)
+    frac_txt = {"resnet50": "1/2.32", "vgg16": "1/5.81", "fcn_resnet101": "1/3",
+                "tiny_cnn": "0.6"}[net.name] if a.budget_frac is None else "%.4f" % a.budget_frac
+
+    log("planning swapped engine (budget %d B) and resident engine" % budget)
+    eng_sw = S.build_engine(net, wts, budget=budget)
+    st = eng_sw.stats()
+    eng_res = S.build_engine(net, wts, budget=st["image_bytes"] + 4096)
+    if a.no_graph:
+        eng_sw.set_option(S.OPT_GRAPH, 0)
+        eng_res.set_option(S.OPT_GRAPH, 0)
+    assert eng_res.stats()["resident"] == 1 and st["resident"] == 0
+
+    xd = torch.from_numpy(x).cuda()
+    yd = torch.empty(eng_sw.out_shape, dtype=torch.float16, device="cuda")
+    yr = torch.empty(eng_sw.out_shape, dtype=torch.float16, device="cuda")
+
+    log("measuring pinned H2D peak")
+    peak = measure_h2d_peak(torch)
+
+    log("timing %d swapped steps" % a.steps)
+    sw_ms, sw_wall = timed_loop(torch, eng_sw, xd, yd, a.steps, a.warmup)
+    log("timing %d resident steps" % a.steps)
+    res_ms, res_wall = timed_loop(torch, eng_res, xd, yr, a.steps, a.warmup)
+    sw_lat = single_latency(torch, eng_sw, xd, yd)
+    res_lat = single_latency(torch, eng_res, xd, yr)
+    sw_host = host_enqueue_us(torch, eng_sw, xd, yd)
+    res_host = host_enqueue_us(torch, eng_res, xd, yr)
+    torch.cuda.synchronize()
+    bitwise = bool(torch.equal(yd.view(torch.int16), yr.view(torch.int16)))
+
+    streamed = st["streamed_bytes"]
+    h2d = streamed / (sw_ms * 1e-3) / 1e9
+    log("timeline and kernel profile (untimed passes)")
+    tl = slab_timeline(S, eng_sw, x)
+    groups = kernel_profile(S, net, eng_res, torch, xd, yr)
+    conv = {k: v for k, v in groups.items() if k.startswith("conv_mfma")}
+    dom = max(conv.items(), key=lambda kv: kv[1][1]) if conv else None
+    total_flops = sum(v[2] for v in groups.values())
+    res_compute_ms = sum(v[1] for v in groups.values())
+    roofline = None
+    if dom:
+        name, (launches, tms, fl, _) = dom
+        ach = fl / (tms * 1e-3) / 1e12
+        roofline = {"bound": "mfma", "kernel": name, "launches_per_step": launches,
+                    "avg_launch_us": round(tms / launches * 1e3, 3),
+                    "achieved": round(ach, 2), "peak": MFMA_FP16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                    "frac": round(ach / MFMA_FP16_PEAK_TFLOPS, 5), "traffic": None}
+    mfma_util = (total_flops / (res_compute_ms * 1e-3) / 1e12) / MFMA_FP16_PEAK_TFLOPS \
+        if res_compute_ms > 0 else None
+
+    out = {
+        "metric": METRIC,
+        "value": round(sw_ms / res_ms, 4),
+        "unit": "x (swapped/resident latency)",
+        "n_gpus": 1, "steps": a.steps, "warmup": a.warmup,
+        "ms_per_step": round(sw_ms, 4),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16 (fp32 accumulate)",
+        "data": "synthetic (seeded He-normal weights, folded BN, N(0,1) input)",
+        "config": {"workload": net.name, "batch": 1, "input": "x".join(map(str, net.input_shape)),
+                   "weight_bytes": net.weight_bytes(), "budget_bytes": budget,
+                   "budget_fraction": frac_txt, "user_blocks": len(net.blocks),
+                   "slabs": st["n_slabs"], "parallelism": "none (1 GPU)"},
+        "swapped_ms": round(sw_ms, 4), "resident_ms": round(res_ms, 4),
+        "swapped_latency_ms": round(sw_lat, 4), "resident_latency_ms": round(res_lat, 4),
+        "swapped_wall_ms": round(sw_wall, 4), "resident_wall_ms": round(res_wall, 4),
+        "host_enqueue_us": {"swapped": round(sw_host, 1), "resident": round(res_host, 1)},
+        "throughput_inf_per_s": round(1e3 / sw_ms, 2),
+        "streamed_bytes_per_step": streamed,
+        "h2d_gbps": round(h2d, 2), "h2d_peak_gbps": round(peak, 2),
+        "h2d_frac": round(h2d / peak, 4),
+        "link": {"bound": "pcie_h2d", "achieved": round(h2d, 2), "peak": round(peak, 2),
+                 "unit": "GB/s", "frac": round(h2d / peak, 4),
+                 "traffic": streamed},
+        "link_floor_ms": round(streamed / (peak * 1e9) * 1e3, 4),
+        "mfma_util": round(mfma_util, 5) if mfma_util else None,
+        "roofline": roofline,
+        "timeline": {k: v for k, v in tl.items() if k != "per_slab" or a.verbose},
+        "kernels": {k: {"launches": v[0], "ms": round(v[1], 4)} for k, v in groups.items()},
+        "swapped_equals_resident_bitwise": bitwise,
+        "activation_bytes": st["activation_bytes"],
+        "hip_graph": not a.no_graph,
+    }
+    if not a.no_cpu_baseline:
+        log("CPU oracle baseline (~%.0f s)" % a.cpu_seconds)
+        out["cpu_baseline"] = cpu_baseline(net, wts, x, a.cpu_seconds)
+    eng_sw.close()
+    eng_res.close()
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

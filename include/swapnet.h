@@ -152,9 +152,25 @@ enum sn_option {
                                    arena budget).  With an arena >= image and
                                    a smaller split budget the run is resident
                                    but has the slabs of the swapped plan      */
-    SN_OPT_TIMING = 2,          /* 1: record per-slab DMA / compute events
-                                   (may be set after plan)                    */
-    SN_OPT_MAX_SLAB = 3         /* cap on slab bytes (0 = none)               */
+    SN_OPT_TIMING = 2,          /* 1: record per-slab DMA / compute events;
+                                   2: also one event pair per layer piece
+                                   (adds launch overhead; for profiling only).
+                                   May be set after plan                      */
+    SN_OPT_MAX_SLAB = 3,        /* cap on slab bytes (0 = none)               */
+    SN_OPT_SWAPIN = 5,          /* how a slab is swapped in: 0 (default) a copy
+                                   kernel on the copy stream reads the pinned
+                                   image through its device mapping (ordering
+                                   by stream barriers, no host round trip);
+                                   1: hipMemcpyAsync (SDMA engine)            */
+    SN_OPT_SWAPIN_BLOCKS = 6,   /* workgroups of the swap-in copy kernel
+                                   (default 128)                              */
+    SN_OPT_GRAPH = 4            /* 1 (default): the kernels of each slab of an
+                                   image network are captured once per
+                                   (input, output) buffer pair into one HIP
+                                   graph per slab and replayed; the swap-in
+                                   DMAs and events stay on the streams.  0:
+                                   launch kernel by kernel.  Not used while
+                                   SN_OPT_TIMING is on, nor for token nets    */
 };
 int sn_set_option(sn_ctx *ctx, int option, int64_t value);
 
@@ -202,6 +218,9 @@ typedef struct sn_slab_info {
     float t_in_ms, t_ex_ms;     /* last inference's DMA and compute time of
                                    this slab (SN_OPT_TIMING), else 0          */
     float t_in_start_ms, t_ex_start_ms; /* start times from inference start   */
+    int32_t wait_slab;          /* this slab's swap-in waits for the compute of
+                                   this earlier slab (-1: none), whose arena
+                                   range it overwrites                         */
 } sn_slab_info;
 int sn_get_slab(const sn_ctx *ctx, int i, sn_slab_info *out);
 
@@ -211,8 +230,13 @@ typedef struct sn_piece_info {
     int32_t kernel;             /* kernel variant chosen for the layer        */
     int64_t w_off, b_off;       /* offsets in the slab (-1 if none)           */
     int64_t w_bytes, b_bytes;
+    float t_ms;                 /* last inference's duration (timing level 2) */
+    int32_t ksplit;             /* K splits of the layer's convolution (1: none) */
 } sn_piece_info;
 int sn_get_piece(const sn_ctx *ctx, int j, sn_piece_info *out);
+
+/* Name of a kernel variant id (as reported in sn_piece_info.kernel), or "?". */
+const char *sn_kernel_name(int kernel);
 
 /* Pinned host image (after sn_plan): pointer and size, for inspection. */
 int sn_get_image(const sn_ctx *ctx, const void **ptr, size_t *bytes);

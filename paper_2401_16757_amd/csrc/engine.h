@@ -41,6 +41,7 @@ struct Layer {
     int64_t w_unit_bytes = 0;  // device weight bytes per unit
     int64_t b_unit_bytes = 0;  // device bias bytes per unit
     int kernel = -1;           // conv tile variant (image convs)
+    int ksplit = 1, kps = 0;   // conv K split (see ConvPlan)
     std::vector<uint16_t> w_dev, b_dev;  // device-layout tensors
 };
 
@@ -56,6 +57,8 @@ struct Slab {
     std::vector<int> pieces;          // indices into Ctx::pieces (after lowering)
     int64_t bytes = 0;
     int64_t image_off = 0, arena_off = 0;
+    int wait = -1;                    // newest earlier slab whose arena range this
+                                      // slab's swap-in overwrites (-1: none)
 };
 
 struct PlanResult {

@@ -39,7 +39,7 @@ struct sn_ctx {
     int n_blocks = 0;
     bool token = false;
     int64_t split_budget = 0, max_slab = 0;
-    bool timing = false;
+    int timing = 0;                    // 1: per slab, 2: also per piece
 
     PlanResult plan;
     std::vector<const void *> piece_w, piece_b;   // bound parameter pointers
@@ -49,6 +49,9 @@ struct sn_ctx {
     uint8_t *arena = nullptr;
     hipStream_t copy_s = nullptr, comp_s = nullptr;
     uint8_t *image = nullptr;          // pinned (device mode) or malloc (host-only)
+    uint8_t *image_dev = nullptr;      // the pinned image as seen from the device
+    int swapin = 0;                    // 0: copy kernel on the copy stream, 1: SDMA
+    int swapin_blocks = 128;
     uint8_t *act = nullptr;
     int64_t act_bytes = 0;
     uint8_t *kv = nullptr;
@@ -59,11 +62,22 @@ struct sn_ctx {
     int32_t *d_ids = nullptr;
     float *q_scratch = nullptr;
     void *in_stage = nullptr, *out_stage = nullptr;
+    float *ws = nullptr;               // split-K partial sums (outside the budget)
+    int64_t ws_bytes = 0;
+
     int64_t in_bytes = 0, out_bytes = 0;
     std::vector<hipEvent_t> loaded, done;
     std::vector<hipEvent_t> t_in0, t_in1, t_ex0, t_ex1;
+    std::vector<hipEvent_t> t_p0, t_p1;   // per-piece events (timing level 2)
+    std::vector<float> piece_ms;
     hipEvent_t t_start = nullptr;
+    hipEvent_t fork = nullptr;         // start of an inference, on the compute stream
+    hipEvent_t ev_end = nullptr;       // end of the previous inference
     bool have_prev = false;
+    bool use_graph = true;             // replay each slab's kernels as one HIP graph
+    std::vector<hipGraphExec_t> graphs;  // per slab, captured for (g_in, g_out)
+    const void *g_in = nullptr;
+    void *g_out = nullptr;
     int pos = 0;
     int64_t n_infers = 0;
     double last_ms = 0;
@@ -160,7 +174,19 @@ extern "C" int sn_set_option(sn_ctx *c, int option, int64_t value) {
         c->split_budget = value;
         return SN_OK;
     case SN_OPT_TIMING:
-        c->timing = value != 0;
+        if (value < 0 || value > 2) return fail(c, SN_E_INVALID, "timing level must be 0, 1 or 2");
+        c->timing = (int)value;
+        return SN_OK;
+    case SN_OPT_SWAPIN:
+        if (value < 0 || value > 1) return fail(c, SN_E_INVALID, "swap-in mode must be 0 or 1");
+        c->swapin = (int)value;
+        return SN_OK;
+    case SN_OPT_SWAPIN_BLOCKS:
+        if (value < 1 || value > 4096) return fail(c, SN_E_INVALID, "swap-in blocks in [1, 4096]");
+        c->swapin_blocks = (int)value;
+        return SN_OK;
+    case SN_OPT_GRAPH:
+        c->use_graph = value != 0;
         return SN_OK;
     case SN_OPT_MAX_SLAB:
         if (c->state != ST_ADDING) return fail(c, SN_E_STATE, "max slab is fixed at plan");
@@ -176,7 +202,12 @@ static void choose_layer_kernels(sn_ctx *c) {
     for (Layer &L : c->layers) {
         if (L.d.op != SN_OP_CONV2D) continue;
         const bool is1x1 = L.d.k == 1 && L.d.pad == 0;
-        L.kernel = conv_kernel_choice(L.out_h * L.out_w, L.d.c_out, L.K, is1x1);
+        const int M = L.out_h * L.out_w;
+        ConvPlan p = conv_plan(M, L.d.c_out, L.K, is1x1, true);
+        L.kernel = p.kernel;
+        L.ksplit = p.ksplit;
+        L.kps = p.kps;
+        c->ws_bytes = std::max(c->ws_bytes, conv_workspace_bytes(p, M, L.d.c_out));
     }
 }
 
@@ -236,10 +267,13 @@ extern "C" int sn_plan(sn_ctx *c) {
     }
 
     HIP_TRY(c, hipHostMalloc((void **)&c->image, (size_t)std::max<int64_t>(c->plan.image_bytes, 1),
-                             hipHostMallocDefault));
+                             hipHostMallocMapped));
+    HIP_TRY(c, hipHostGetDevicePointer((void **)&c->image_dev, c->image, 0));
     write_image(c->layers, c->plan, c->image);
     HIP_TRY(c, hipMalloc((void **)&c->act, (size_t)std::max<int64_t>(c->act_bytes, kAlign)));
     HIP_TRY(c, hipMemset(c->act, 0, (size_t)std::max<int64_t>(c->act_bytes, kAlign)));
+    if (c->ws_bytes) HIP_TRY(c, hipMalloc((void **)&c->ws, (size_t)c->ws_bytes));
+
     if (c->token) {
         c->table_bytes = (int64_t)first.w_dev.size() * 2;
         HIP_TRY(c, hipHostMalloc(&c->table_host, (size_t)c->table_bytes, hipHostMallocMapped));
@@ -287,6 +321,15 @@ extern "C" int sn_plan(sn_ctx *c) {
         HIP_TRY(c, hipEventCreate(&c->t_ex1[i]));
     }
     HIP_TRY(c, hipEventCreate(&c->t_start));
+    HIP_TRY(c, hipEventCreateWithFlags(&c->fork, hipEventDisableTiming));
+    HIP_TRY(c, hipEventCreateWithFlags(&c->ev_end, hipEventDisableTiming));
+    c->t_p0.assign(np, nullptr);
+    c->t_p1.assign(np, nullptr);
+    for (int j = 0; j < np; ++j) {
+        HIP_TRY(c, hipEventCreate(&c->t_p0[j]));
+        HIP_TRY(c, hipEventCreate(&c->t_p1[j]));
+    }
+    c->piece_ms.assign(np, 0.f);
     c->slab_t_in.assign(ns, 0.f);
     c->slab_t_ex.assign(ns, 0.f);
     c->slab_t_in_start.assign(ns, 0.f);
@@ -336,7 +379,12 @@ static int run_piece(sn_ctx *c, int pi, int n_tok, hipStream_t s) {
         a.ldy = L.cout_p;
         a.n_zero_end = p.u1 == L.units ? L.cout_p : (int)p.u1;
         a.relu = (d.flags & SN_FLAG_RELU) ? 1 : 0;
-        e = launch_conv(L.kernel, a, s);
+        a.ws = c->ws;
+        ConvPlan cp;
+        cp.kernel = L.kernel;
+        cp.ksplit = L.ksplit;
+        cp.kps = L.kps;
+        e = launch_conv(cp, a, s);
         break;
     }
     case SN_OP_LINEAR: {
@@ -387,8 +435,8 @@ static int run_piece(sn_ctx *c, int pi, int n_tok, hipStream_t s) {
             a.relu = (d.flags & SN_FLAG_RELU) ? 1 : 0;
             a.swiglu = swiglu;
             // tile chosen from the whole layer, never from the piece
-            int kern = conv_kernel_choice(M, (int)L.units * L.rows_per_unit, L.K, true);
-            e = launch_conv(kern, a, s);
+            ConvPlan cp = conv_plan(M, (int)L.units * L.rows_per_unit, L.K, true, false);
+            e = launch_conv(cp, a, s);
         }
         break;
     }
@@ -425,51 +473,74 @@ static int run_piece(sn_ctx *c, int pi, int n_tok, hipStream_t s) {
     return SN_OK;
 }
 
-// Swap-in of slab i on the copy stream.  Slab i reuses the arena range of
-// slab i-2 (two-ended placement), so it waits for that slab's compute.  The
-// first two slabs of an inference wait for the last slab of the previous
-// inference that used the same end of the arena.
+// Swap-in of slab i on the copy stream.  It overwrites arena bytes last used
+// by slab `wait` (the newest earlier slab overlapping its range), so it waits
+// for that slab's compute; a slab with no such predecessor waits only for
+// the start of the inference, which follows the previous inference.
 static int enqueue_copy(sn_ctx *c, int i) {
     const Slab &s = c->plan.slabs[i];
-    const int ns = (int)c->plan.slabs.size();
-    if (i >= 2) {
-        HIP_TRY(c, hipStreamWaitEvent(c->copy_s, c->done[i - 2], 0));
-    } else if (c->have_prev) {
-        int last_same = (ns - 1) - (((ns - 1) - i) % 2);
-        HIP_TRY(c, hipStreamWaitEvent(c->copy_s, c->done[last_same], 0));
-    }
+    HIP_TRY(c, hipStreamWaitEvent(c->copy_s, s.wait >= 0 ? c->done[s.wait] : c->fork, 0));
     if (c->timing) HIP_TRY(c, hipEventRecord(c->t_in0[i], c->copy_s));
-    if (s.bytes)
-        HIP_TRY(c, hipMemcpyAsync(c->arena + s.arena_off, c->image + s.image_off, (size_t)s.bytes,
-                                  hipMemcpyHostToDevice, c->copy_s));
+    if (s.bytes) {
+        if (c->swapin == 1)
+            HIP_TRY(c, hipMemcpyAsync(c->arena + s.arena_off, c->image + s.image_off,
+                                      (size_t)s.bytes, hipMemcpyHostToDevice, c->copy_s));
+        else
+            HIP_TRY(c, launch_swapin(c->image_dev + s.image_off, c->arena + s.arena_off, s.bytes,
+                                     c->swapin_blocks, c->copy_s));
+    }
     if (c->timing) HIP_TRY(c, hipEventRecord(c->t_in1[i], c->copy_s));
     HIP_TRY(c, hipEventRecord(c->loaded[i], c->copy_s));
     return SN_OK;
 }
 
-static int run_network(sn_ctx *c, int n_tok, hipStream_t cs) {
+// Kernels of slab i (its layer pieces), enqueued on `cs`.
+static int slab_kernels(sn_ctx *c, int i, int n_tok, hipStream_t cs) {
+    int rc;
+    for (int pi : c->plan.slabs[i].pieces) {
+        if (c->timing >= 2) HIP_TRY(c, hipEventRecord(c->t_p0[pi], cs));
+        if ((rc = run_piece(c, pi, n_tok, cs))) return rc;
+        if (c->timing >= 2) HIP_TRY(c, hipEventRecord(c->t_p1[pi], cs));
+    }
+    return SN_OK;
+}
+
+// One pass over all slabs: swap-in on the copy stream, compute on `cs`.
+// `pre` / `post` run on `cs` around the first / last slab's kernels (input
+// and output conversion).  With `graphs`, slab i's kernels (with pre / post
+// for the first / last slab) are replayed from graphs[i] instead.
+template <typename Pre, typename Post>
+static int run_slabs(sn_ctx *c, int n_tok, hipStream_t cs, Pre pre, Post post, bool graphs) {
     const int ns = (int)c->plan.slabs.size();
     const bool swap = !c->plan.resident;
     int rc;
     if (c->timing) HIP_TRY(c, hipEventRecord(c->t_start, cs));
-    if (swap) {
-        // the copy stream must not run ahead of work the caller queued earlier
-        // on `cs` that may still read activations of a previous inference
-        for (int i = 0; i < std::min(ns, 2); ++i)
-            if ((rc = enqueue_copy(c, i))) return rc;
-    }
+    HIP_TRY(c, hipEventRecord(c->fork, cs));
+    // copies are issued in slab order, each as soon as the compute it waits
+    // for has been enqueued
+    int next_copy = 0;
+    auto issue = [&](int done_upto) -> int {
+        while (swap && next_copy < ns && c->plan.slabs[next_copy].wait <= done_upto) {
+            int r = enqueue_copy(c, next_copy++);
+            if (r) return r;
+        }
+        return SN_OK;
+    };
+    if ((rc = issue(-1))) return rc;
     for (int i = 0; i < ns; ++i) {
-        const Slab &s = c->plan.slabs[i];
         if (swap) HIP_TRY(c, hipStreamWaitEvent(cs, c->loaded[i], 0));
         if (c->timing) HIP_TRY(c, hipEventRecord(c->t_ex0[i], cs));
-        for (int pi : s.pieces)
-            if ((rc = run_piece(c, pi, n_tok, cs))) return rc;
+        if (graphs) {
+            HIP_TRY(c, hipGraphLaunch(c->graphs[i], cs));
+        } else {
+            if (i == 0 && (rc = pre(cs))) return rc;
+            if ((rc = slab_kernels(c, i, n_tok, cs))) return rc;
+            if (i == ns - 1 && (rc = post(cs))) return rc;
+        }
         if (c->timing) HIP_TRY(c, hipEventRecord(c->t_ex1[i], cs));
         HIP_TRY(c, hipEventRecord(c->done[i], cs));
-        if (swap && i + 2 < ns)
-            if ((rc = enqueue_copy(c, i + 2))) return rc;
+        if ((rc = issue(i))) return rc;
     }
-    c->have_prev = true;
     return SN_OK;
 }
 
@@ -489,6 +560,12 @@ static void collect_timing(sn_ctx *c) {
         c->slab_t_in_start[i] = x;
         c->slab_t_ex_start[i] = y;
     }
+    if (c->timing >= 2)
+        for (size_t j = 0; j < c->piece_ms.size(); ++j) {
+            float t = 0;
+            hipEventElapsedTime(&t, c->t_p0[j], c->t_p1[j]);
+            c->piece_ms[j] = t;
+        }
 }
 
 static int check_ready(sn_ctx *c, bool token) {
@@ -500,24 +577,86 @@ static int check_ready(sn_ctx *c, bool token) {
     return SN_OK;
 }
 
-static int infer_dev_impl(sn_ctx *c, const void *d_in, void *d_out, hipStream_t cs) {
+// Input conversion (before the first slab's kernels) and output conversion
+// (after the last slab's) of an image network.
+static int convert_input(sn_ctx *c, const void *d_in, hipStream_t cs) {
     const Layer &first = c->layers[0];
     const Slot &ins = c->slots[first.d.src];
     hipError_t e;
     if (ins.h * ins.w > 1 || ins.cp != ins.c)
         e = launch_chw_to_hwc(d_in, slot_ptr(c, first.d.src), ins.c, ins.h, ins.w, ins.cp, cs);
     else
-        e = hipMemcpyAsync(slot_ptr(c, first.d.src), d_in, (size_t)ins.c * 2, hipMemcpyDeviceToDevice, cs);
+        e = hipMemcpyAsync(slot_ptr(c, first.d.src), d_in, (size_t)ins.c * 2,
+                           hipMemcpyDeviceToDevice, cs);
     if (e != hipSuccess) return fail(c, SN_E_HIP, std::string("input: ") + hipGetErrorString(e));
-    int rc = run_network(c, 1, cs);
-    if (rc) return rc;
-    const Slot &o = c->slots[c->layers.back().d.dst];
+    return SN_OK;
+}
+
+static int convert_output(sn_ctx *c, void *d_out, hipStream_t cs) {
+    const int out_slot = c->layers.back().d.dst;
+    const Slot &o = c->slots[out_slot];
+    hipError_t e;
     if (o.h * o.w > 1)
-        e = launch_hwc_to_chw(slot_ptr(c, c->layers.back().d.dst), d_out, o.c, o.h, o.w, o.cp, cs);
+        e = launch_hwc_to_chw(slot_ptr(c, out_slot), d_out, o.c, o.h, o.w, o.cp, cs);
     else
-        e = hipMemcpyAsync(d_out, slot_ptr(c, c->layers.back().d.dst), (size_t)o.c * o.elem,
+        e = hipMemcpyAsync(d_out, slot_ptr(c, out_slot), (size_t)o.c * o.elem,
                            hipMemcpyDeviceToDevice, cs);
     if (e != hipSuccess) return fail(c, SN_E_HIP, std::string("output: ") + hipGetErrorString(e));
+    return SN_OK;
+}
+
+static void drop_graphs(sn_ctx *c) {
+    for (hipGraphExec_t g : c->graphs)
+        if (g) hipGraphExecDestroy(g);
+    c->graphs.clear();
+}
+
+// Capture each slab's kernels into its own graph for these buffers.  Only
+// kernels are captured: the swap-in DMAs stay on the copy stream (SDMA) and
+// the ordering events stay outside the graphs.
+static int capture_graphs(sn_ctx *c, const void *d_in, void *d_out) {
+    drop_graphs(c);
+    const int ns = (int)c->plan.slabs.size();
+    c->graphs.assign(ns, nullptr);
+    for (int i = 0; i < ns; ++i) {
+        HIP_TRY(c, hipStreamBeginCapture(c->comp_s, hipStreamCaptureModeRelaxed));
+        int rc = SN_OK;
+        if (i == 0) rc = convert_input(c, d_in, c->comp_s);
+        if (!rc) rc = slab_kernels(c, i, 1, c->comp_s);
+        if (!rc && i == ns - 1) rc = convert_output(c, d_out, c->comp_s);
+        hipGraph_t g = nullptr;
+        hipError_t e = hipStreamEndCapture(c->comp_s, &g);
+        if (!rc && e != hipSuccess)
+            rc = fail(c, SN_E_HIP, std::string("graph capture: ") + hipGetErrorString(e));
+        if (!rc) {
+            e = hipGraphInstantiate(&c->graphs[i], g, nullptr, nullptr, 0);
+            if (e != hipSuccess)
+                rc = fail(c, SN_E_HIP, std::string("graph instantiate: ") + hipGetErrorString(e));
+        }
+        if (g) hipGraphDestroy(g);
+        if (rc) {
+            drop_graphs(c);
+            return rc;
+        }
+    }
+    c->g_in = d_in;
+    c->g_out = d_out;
+    return SN_OK;
+}
+
+static int infer_dev_impl(sn_ctx *c, const void *d_in, void *d_out, hipStream_t cs) {
+    // inferences are serialised: activations and arena are shared
+    if (c->have_prev) HIP_TRY(c, hipStreamWaitEvent(cs, c->ev_end, 0));
+    const bool graphs = c->use_graph && !c->timing;
+    int rc;
+    if (graphs && (c->graphs.empty() || c->g_in != d_in || c->g_out != d_out))
+        if ((rc = capture_graphs(c, d_in, d_out))) return rc;
+    rc = run_slabs(
+        c, 1, cs, [&](hipStream_t s) { return convert_input(c, d_in, s); },
+        [&](hipStream_t s) { return convert_output(c, d_out, s); }, graphs);
+    if (rc) return rc;
+    HIP_TRY(c, hipEventRecord(c->ev_end, cs));
+    c->have_prev = true;
     c->n_infers++;
     return SN_OK;
 }
@@ -561,8 +700,10 @@ extern "C" int sn_infer_tokens(sn_ctx *c, const int32_t *ids, int n_ids, float *
         if (ids[i] < 0 || ids[i] >= vocab) return fail(c, SN_E_INVALID, "token id out of range");
     auto t0 = std::chrono::steady_clock::now();
     hipStream_t cs = c->comp_s;
+    if (c->have_prev) HIP_TRY(c, hipStreamWaitEvent(cs, c->ev_end, 0));
     HIP_TRY(c, hipMemcpyAsync(c->d_ids, ids, (size_t)n_ids * 4, hipMemcpyHostToDevice, cs));
-    rc = run_network(c, n_ids, cs);
+    auto none = [](hipStream_t) { return (int)SN_OK; };
+    rc = run_slabs(c, n_ids, cs, none, none, false);
     if (rc) {
         hipStreamSynchronize(cs);
         hipStreamSynchronize(c->copy_s);
@@ -570,6 +711,8 @@ extern "C" int sn_infer_tokens(sn_ctx *c, const int32_t *ids, int n_ids, float *
     }
     HIP_TRY(c, hipMemcpyAsync(logits, slot_ptr(c, c->layers.back().d.dst), (size_t)c->out_bytes,
                               hipMemcpyDeviceToHost, cs));
+    HIP_TRY(c, hipEventRecord(c->ev_end, cs));
+    c->have_prev = true;
     HIP_TRY(c, hipStreamSynchronize(cs));
     collect_timing(c);
     c->pos += n_ids;
@@ -597,7 +740,7 @@ extern "C" int sn_get_stats(const sn_ctx *c, sn_stats *o) {
     o->image_bytes = c->plan.image_bytes;
     o->arena_high_water = c->plan.high_water;
     o->streamed_bytes = c->plan.resident ? 0 : c->plan.image_bytes;
-    o->activation_bytes = c->act_bytes;
+    o->activation_bytes = c->act_bytes + c->ws_bytes;
     o->kv_bytes = c->kv_bytes;
     o->table_bytes = (int64_t)(c->plan.pieces.size() * sizeof(Piece) + c->plan.slabs.size() * sizeof(Slab) +
                                c->piece_w.size() * 2 * sizeof(void *) + c->layers.size() * sizeof(Layer));
@@ -619,6 +762,7 @@ extern "C" int sn_get_slab(const sn_ctx *c, int i, sn_slab_info *o) {
     o->arena_off = s.arena_off;
     o->bytes = s.bytes;
     o->first_piece = s.pieces.empty() ? -1 : s.pieces.front();
+    o->wait_slab = s.wait;
     o->n_pieces = (int32_t)s.pieces.size();
     if (i < (int)c->slab_t_in.size()) {
         o->t_in_ms = c->slab_t_in[i];
@@ -642,6 +786,8 @@ extern "C" int sn_get_piece(const sn_ctx *c, int j, sn_piece_info *o) {
     o->b_off = p.b_off;
     o->w_bytes = p.w_bytes;
     o->b_bytes = p.b_bytes;
+    o->t_ms = j < (int)c->piece_ms.size() ? c->piece_ms[j] : 0.f;
+    o->ksplit = c->layers[p.layer].ksplit;
     return SN_OK;
 }
 
@@ -653,6 +799,8 @@ extern "C" int sn_get_image(const sn_ctx *c, const void **ptr, size_t *bytes) {
     return SN_OK;
 }
 
+extern "C" const char *sn_kernel_name(int kernel) { return conv_kernel_name(kernel); }
+
 extern "C" const char *sn_last_error(const sn_ctx *c) {
     if (!c) return g_create_err.c_str();
     return c->err.c_str();
@@ -663,14 +811,18 @@ extern "C" void sn_destroy(sn_ctx *c) {
     if (!c->host_only) {
         if (c->comp_s) hipStreamSynchronize(c->comp_s);
         if (c->copy_s) hipStreamSynchronize(c->copy_s);
-        for (auto *v : {&c->loaded, &c->done, &c->t_in0, &c->t_in1, &c->t_ex0, &c->t_ex1})
+        for (auto *v : {&c->loaded, &c->done, &c->t_in0, &c->t_in1, &c->t_ex0, &c->t_ex1, &c->t_p0,
+                        &c->t_p1})
             for (hipEvent_t e : *v)
                 if (e) hipEventDestroy(e);
         if (c->t_start) hipEventDestroy(c->t_start);
+        if (c->fork) hipEventDestroy(c->fork);
+        if (c->ev_end) hipEventDestroy(c->ev_end);
+        drop_graphs(c);
         if (c->image) hipHostFree(c->image);
         if (c->table_host) hipHostFree(c->table_host);
         for (void *p : {(void *)c->arena, (void *)c->act, (void *)c->kv, (void *)c->d_ids,
-                        (void *)c->q_scratch, c->in_stage, c->out_stage})
+                        (void *)c->q_scratch, c->in_stage, c->out_stage, (void *)c->ws})
             if (p) hipFree(p);
         if (c->copy_s) hipStreamDestroy(c->copy_s);
         if (c->comp_s) hipStreamDestroy(c->comp_s);

@@ -30,6 +30,22 @@ struct ConvArgs {
     int ldy;            // channel stride of y and res
     int n_zero_end;     // zero output channels [n0 + units, n_zero_end) (padding)
     int relu, swiglu;
+    // split-K: blockIdx.y = split s covers k in [s*kps, (s+1)*kps); with
+    // ksplit > 1 each block writes its partial sums to ws[s][m][n] (fp32)
+    // and a second kernel adds them in split order 0..ksplit-1 and applies
+    // the epilogue
+    int ksplit, kps;
+    float *ws;
+    int n_cover;        // columns covered by the tile grid (>= N, includes padding)
+};
+
+// How a convolution layer is computed: tile variant and K split, chosen from
+// the whole layer's (M, N, K) so that every slab piece of the layer runs the
+// same reduction order.
+struct ConvPlan {
+    int kernel = -1;
+    int ksplit = 1;
+    int kps = 0;
 };
 
 // Matrix-vector product for batch-1 linear layers (HBM-bound):
@@ -49,10 +65,11 @@ struct GemvArgs {
     int zero_end;       // if > n0 + units: zero outputs [n0 + units, zero_end)
 };
 
-int conv_kernel_choice(int M, int N, int K, bool is1x1);
+ConvPlan conv_plan(int M, int N, int K, bool is1x1, bool allow_split);
+int64_t conv_workspace_bytes(const ConvPlan &p, int M, int N);
 int conv_kernel_count();
 const char *conv_kernel_name(int id);
-hipError_t launch_conv(int kernel, const ConvArgs &a, hipStream_t s);
+hipError_t launch_conv(const ConvPlan &p, ConvArgs a, hipStream_t s);
 hipError_t launch_gemv(const GemvArgs &a, hipStream_t s);
 
 hipError_t launch_maxpool(const void *x, void *y, int H, int W, int Cp, int Ho, int Wo, int k,
@@ -61,6 +78,13 @@ hipError_t launch_gavgpool(const void *x, void *y, int HW, int Cp, hipStream_t s
 hipError_t launch_upsample(const void *x, void *y, int H, int W, int Cp, int scale, hipStream_t s);
 hipError_t launch_chw_to_hwc(const void *x, void *y, int C, int H, int W, int Cp, hipStream_t s);
 hipError_t launch_hwc_to_chw(const void *x, void *y, int C, int H, int W, int Cp, hipStream_t s);
+
+// Swap-in by the compute units: copy `bytes` (a multiple of 16) from pinned
+// host memory mapped into the device address space into device memory.
+// Ordering against other streams then uses ordinary stream barriers, with no
+// host involvement.
+hipError_t launch_swapin(const void *src_host_mapped, void *dst, int64_t bytes, int blocks,
+                         hipStream_t s);
 
 hipError_t launch_embed(const int32_t *ids, const void *table, void *y, int T, int d, hipStream_t s);
 hipError_t launch_rmsnorm(const void *x, const void *gain, void *y, int T, int d, float eps,

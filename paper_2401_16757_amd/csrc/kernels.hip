@@ -13,6 +13,8 @@
 
 #include <math.h>
 
+#include <algorithm>
+
 namespace sn {
 
 typedef _Float16 h8 __attribute__((ext_vector_type(8)));
@@ -62,7 +64,7 @@ __global__ __launch_bounds__(WM *WN * 64) void conv_mfma_kernel(ConvArgs a) {
 
     // Tile coordinates; blockIdx.x walks N tiles fastest so that consecutive
     // blocks share the same activation rows.
-    const int n_tiles = (a.N + BN - 1) / BN;
+    const int n_tiles = (a.n_cover + BN - 1) / BN;
     const int tile_m = blockIdx.x / n_tiles;
     const int tile_n = blockIdx.x % n_tiles;
     const int m0 = tile_m * BM, nb0 = tile_n * BN;
@@ -132,12 +134,14 @@ __global__ __launch_bounds__(WM *WN * 64) void conv_mfma_kernel(ConvArgs a) {
     const int lrow = lane & 31;
     const int lk = (lane >> 5) * 8;
 
-    load_tile(0);
-    for (int k0 = 0; k0 < a.K; k0 += BK) {
+    const int kbeg = blockIdx.y * a.kps;
+    const int kend = min(a.K, kbeg + a.kps);
+    load_tile(kbeg);
+    for (int k0 = kbeg; k0 < kend; k0 += BK) {
         __syncthreads();
         store_tile();
         __syncthreads();
-        if (k0 + BK < a.K) load_tile(k0 + BK);
+        if (k0 + BK < kend) load_tile(k0 + BK);
 #pragma unroll
         for (int kk = 0; kk < BK; kk += 16) {
             h8 fa[TM], fb[TN];
@@ -154,6 +158,23 @@ __global__ __launch_bounds__(WM *WN * 64) void conv_mfma_kernel(ConvArgs a) {
                     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fa[i], fb[j], acc[i][j],
                                                                         0, 0, 0);
         }
+    }
+
+    if (a.ksplit > 1) {
+        // partial sums of this K split; splitk_reduce_kernel adds them
+        float *ws = a.ws + (long)blockIdx.y * a.M * a.N;
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+                const int n = nb0 + wn * WTN + j * 32 + lrow;
+#pragma unroll
+                for (int v = 0; v < 16; ++v) {
+                    const int m = m0 + wm * WTM + i * 32 + (v >> 2) * 8 + (lane >> 5) * 4 + (v & 3);
+                    if (m < a.M && n < a.N) ws[(long)m * a.N + n] = acc[i][j][v];
+                }
+            }
+        return;
     }
 
     // Epilogue: bias, residual, ReLU / SwiGLU, one rounding to fp16.
@@ -223,33 +244,92 @@ const char *conv_kernel_name(int id) {
     return (id >= 0 && id < kNumConvVariants) ? kConvVariants[id].name : "?";
 }
 
-// Tile choice from the full layer shape (never from a slab's channel range):
-// the largest tile that still gives every CU a block, else the one with most
-// blocks.
-int conv_kernel_choice(int M, int N, int K, bool is1x1) {
-    const int cus = 256;
-    int best = -1;
-    long best_blocks = -1;
-    for (int id = 0; id < kNumConvVariants; ++id) {
-        const ConvVariant &v = kConvVariants[id];
-        if (v.is1x1 != is1x1) continue;
-        long blocks = (long)((M + v.bm - 1) / v.bm) * ((N + v.bn - 1) / v.bn);
-        if (blocks >= cus) return id;
-        if (blocks > best_blocks) {
-            best_blocks = blocks;
-            best = id;
-        }
+// Sum of the K-split partials in split order 0..ksplit-1, then bias,
+// residual, ReLU and the fp16 rounding; also zeroes the output's padding
+// channels.  A separate kernel: the kernel boundary orders the partial-sum
+// writes of all splits (on any XCD) before these reads.
+__global__ void splitk_reduce_kernel(ConvArgs a) {
+    long t = (long)blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= (long)a.M * a.n_cover) return;
+    const int m = (int)(t / a.n_cover), n = (int)(t - (long)m * a.n_cover);
+    _Float16 *yg = (_Float16 *)a.y;
+    const long idx = (long)m * a.ldy + a.n0 + n;
+    if (n >= a.N) {
+        if (a.n0 + n < a.n_zero_end) yg[idx] = (_Float16)0.0f;
+        return;
     }
-    (void)K;
-    return best;
+    const long plane = (long)a.M * a.N;
+    const float *p = a.ws + (long)m * a.N + n;
+    float v = 0.0f;
+    for (int s = 0; s < a.ksplit; ++s) v += p[s * plane];
+    if (a.bias) v += (float)((const _Float16 *)a.bias)[n];
+    if (a.res) v += (float)((const _Float16 *)a.res)[idx];
+    if (a.relu) v = fmaxf(v, 0.0f);
+    yg[idx] = (_Float16)v;
 }
 
-hipError_t launch_conv(int kernel, const ConvArgs &a, hipStream_t s) {
-    if (kernel < 0 || kernel >= kNumConvVariants) return hipErrorInvalidValue;
-    const ConvVariant &v = kConvVariants[kernel];
+static int find_variant(int bm, int bn, bool is1x1) {
+    for (int id = 0; id < kNumConvVariants; ++id)
+        if (kConvVariants[id].bm == bm && kConvVariants[id].bn == bn &&
+            kConvVariants[id].is1x1 == is1x1)
+            return id;
+    return -1;
+}
+
+// Tile and K split from the whole layer's shape (never from a slab's channel
+// range): the largest 4-wave tile that gives every CU a block; otherwise
+// 64 x 64 tiles with the K range split so that about 256 blocks run, each
+// over at least four K tiles.
+ConvPlan conv_plan(int M, int N, int K, bool is1x1, bool allow_split) {
+    const int target = 256;
+    ConvPlan p;
+    static const int tiles[][2] = {{128, 128}, {128, 64}, {64, 128}, {64, 64}};
+    for (auto &t : tiles) {
+        long blocks = (long)((M + t[0] - 1) / t[0]) * ((N + t[1] - 1) / t[1]);
+        if (blocks >= target - 16) {
+            p.kernel = find_variant(t[0], t[1], is1x1);
+            p.kps = K;
+            return p;
+        }
+    }
+    p.kernel = find_variant(64, 64, is1x1);
+    const ConvVariant &v = kConvVariants[p.kernel];
+    long blocks = (long)((M + 63) / 64) * ((N + 63) / 64);
+    const int kt = (K + v.bk - 1) / v.bk;
+    int s = allow_split ? (int)std::min<long>((target + blocks - 1) / blocks, kt / 4) : 1;
+    if (s < 2) {
+        p.kps = K;
+        return p;
+    }
+    const int per = (kt + s - 1) / s;
+    p.kps = per * v.bk;
+    p.ksplit = (K + p.kps - 1) / p.kps;
+    if (p.ksplit < 2) {
+        p.ksplit = 1;
+        p.kps = K;
+    }
+    return p;
+}
+
+int64_t conv_workspace_bytes(const ConvPlan &p, int M, int N) {
+    return p.ksplit > 1 ? (int64_t)p.ksplit * M * N * 4 : 0;
+}
+
+
+hipError_t launch_conv(const ConvPlan &p, ConvArgs a, hipStream_t s) {
+    if (p.kernel < 0 || p.kernel >= kNumConvVariants) return hipErrorInvalidValue;
+    const ConvVariant &v = kConvVariants[p.kernel];
     if (a.M <= 0 || a.N <= 0) return hipSuccess;
-    long blocks = (long)((a.M + v.bm - 1) / v.bm) * ((a.N + v.bn - 1) / v.bn);
-    hipLaunchKernelGGL(v.fn, dim3((unsigned)blocks), dim3(v.threads), 0, s, a);
+    a.ksplit = p.ksplit;
+    a.kps = p.ksplit > 1 ? p.kps : a.K;
+    if (a.ksplit > 1 && (!a.ws || a.swiglu)) return hipErrorInvalidValue;
+    a.n_cover = std::max(a.N, a.n_zero_end - a.n0);
+    long blocks = (long)((a.M + v.bm - 1) / v.bm) * ((a.n_cover + v.bn - 1) / v.bn);
+    hipLaunchKernelGGL(v.fn, dim3((unsigned)blocks, (unsigned)a.ksplit), dim3(v.threads), 0, s, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || a.ksplit == 1) return e;
+    long n = (long)a.M * a.n_cover;
+    hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, a);
     return hipGetLastError();
 }
 
@@ -485,6 +565,41 @@ hipError_t launch_hwc_to_chw(const void *x, void *y, int C, int H, int W, int Cp
     long n = (long)H * W * C;
     hipLaunchKernelGGL(hwc_to_chw_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s,
                        (const _Float16 *)x, (_Float16 *)y, C, H * W, Cp);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Swap-in copy kernel: each thread keeps four 16-byte host reads in flight;
+// reads are non-temporal (the image is read once per inference).
+// ---------------------------------------------------------------------------
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+__global__ __launch_bounds__(256) void swapin_kernel(const u32x4 *__restrict__ src,
+                                                     u32x4 *__restrict__ dst, long n16) {
+    const long stride = (long)gridDim.x * 256;
+    long i = (long)blockIdx.x * 256 + threadIdx.x;
+    for (; i + 3 * stride < n16; i += 4 * stride) {
+        u32x4 a = __builtin_nontemporal_load(src + i);
+        u32x4 b = __builtin_nontemporal_load(src + i + stride);
+        u32x4 c = __builtin_nontemporal_load(src + i + 2 * stride);
+        u32x4 d = __builtin_nontemporal_load(src + i + 3 * stride);
+        dst[i] = a;
+        dst[i + stride] = b;
+        dst[i + 2 * stride] = c;
+        dst[i + 3 * stride] = d;
+    }
+    for (; i < n16; i += stride) dst[i] = __builtin_nontemporal_load(src + i);
+}
+
+hipError_t launch_swapin(const void *src_host_mapped, void *dst, int64_t bytes, int blocks,
+                         hipStream_t s) {
+    if (bytes <= 0) return hipSuccess;
+    if (bytes % 16) return hipErrorInvalidValue;
+    const long n16 = bytes / 16;
+    long need = (n16 + 1023) / 1024;   // at least 4 chunks per thread
+    unsigned grid = (unsigned)std::max<long>(1, std::min<long>(blocks, need));
+    hipLaunchKernelGGL(swapin_kernel, dim3(grid), dim3(256), 0, s, (const u32x4 *)src_host_mapped,
+                       (u32x4 *)dst, n16);
     return hipGetLastError();
 }
 

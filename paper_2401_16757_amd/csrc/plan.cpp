@@ -473,6 +473,14 @@ int plan_slabs(const std::vector<Layer> &layers, int n_blocks, int64_t split_bud
     return SN_OK;
 }
 
+// Arena placement.  The pair constraint (Eq. 3) guarantees that slab i and
+// slab i+1 fit side by side at the two ends of the arena; within that
+// guarantee each slab is put where its swap-in has to wait for the oldest
+// possible earlier slab, so that small slabs let the DMA run several slabs
+// ahead of the compute (the m = 2 parallel blocks of Sec. 6.2.2 are the
+// floor, not the ceiling).  A position in the middle of the arena is taken
+// only if the next slab still fits at one of the two ends beside it, which
+// keeps every later placement feasible.
 int place_slabs(PlanResult &p, int64_t arena_budget, std::string &err) {
     const int64_t B = arena_budget / kAlign * kAlign;
     const int n = (int)p.slabs.size();
@@ -481,6 +489,7 @@ int place_slabs(PlanResult &p, int64_t arena_budget, std::string &err) {
         int64_t off = 0;
         for (Slab &s : p.slabs) {
             s.arena_off = off;
+            s.wait = -1;
             off += s.bytes;
         }
         p.high_water = off;
@@ -488,6 +497,9 @@ int place_slabs(PlanResult &p, int64_t arena_budget, std::string &err) {
     }
     p.resident = false;
     p.high_water = 0;
+    auto overlap = [](int64_t a, int64_t sa, int64_t b, int64_t sb) {
+        return sa > 0 && sb > 0 && a < b + sb && b < a + sa;
+    };
     for (int i = 0; i < n; ++i) {
         Slab &s = p.slabs[i];
         if (s.bytes > B || (i + 1 < n && s.bytes + p.slabs[i + 1].bytes > B)) {
@@ -495,9 +507,36 @@ int place_slabs(PlanResult &p, int64_t arena_budget, std::string &err) {
                   " do not fit the arena together";
             return SN_E_INFEASIBLE;
         }
-        // two-ended arena: even slabs from the bottom, odd slabs from the top,
-        // so consecutive slabs are disjoint exactly when the pair fits
-        s.arena_off = (i % 2 == 0) ? 0 : B - s.bytes;
+        std::vector<int64_t> cand = {0, B - s.bytes};
+        for (int j = 0; j < i; ++j) {
+            cand.push_back(p.slabs[j].arena_off + p.slabs[j].bytes);
+            cand.push_back(p.slabs[j].arena_off - s.bytes);
+        }
+        const int64_t next = i + 1 < n ? p.slabs[i + 1].bytes : 0;
+        int best_wait = 1 << 30;
+        int64_t best_off = -1;
+        for (int64_t c : cand) {
+            if (c < 0 || c + s.bytes > B || c % kAlign) continue;
+            if (i > 0 && overlap(c, s.bytes, p.slabs[i - 1].arena_off, p.slabs[i - 1].bytes)) continue;
+            const bool at_end = c == 0 || c == B - s.bytes;
+            if (!at_end && next > 0 && !(next <= c || c + s.bytes + next <= B)) continue;
+            int w = -1;
+            for (int j = i - 1; j >= 0; --j)
+                if (overlap(c, s.bytes, p.slabs[j].arena_off, p.slabs[j].bytes)) {
+                    w = j;
+                    break;
+                }
+            if (w < best_wait || (w == best_wait && c < best_off)) {
+                best_wait = w;
+                best_off = c;
+            }
+        }
+        if (best_off < 0) {
+            err = "placement failed for slab " + std::to_string(i);
+            return SN_E_INFEASIBLE;
+        }
+        s.arena_off = best_off;
+        s.wait = best_wait;
         p.high_water = std::max(p.high_water, s.arena_off + s.bytes);
     }
     return SN_OK;

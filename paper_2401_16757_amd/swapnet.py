@@ -26,11 +26,11 @@ OP = {"conv2d": 1, "linear": 2, "maxpool": 3, "gavgpool": 4, "upsample_bilinear"
       "embed": 6, "rmsnorm": 7, "attention": 8}
 FLAG_RELU, FLAG_FLATTEN_CHW, FLAG_SWIGLU, FLAG_OUT_F32, FLAG_LAST_ROW = 1, 2, 4, 8, 16
 CREATE_HOST_ONLY = 1
-OPT_SPLIT_BUDGET, OPT_TIMING, OPT_MAX_SLAB = 1, 2, 3
+OPT_SPLIT_BUDGET, OPT_TIMING, OPT_MAX_SLAB, OPT_GRAPH, OPT_SWAPIN, OPT_SWAPIN_BLOCKS = 1, 2, 3, 4, 5, 6
 
 EXPORTS = ["sn_create", "sn_create_ex", "sn_add_block", "sn_plan", "sn_set_option", "sn_infer",
            "sn_infer_dev", "sn_infer_tokens", "sn_reset", "sn_get_stats", "sn_get_slab",
-           "sn_get_piece", "sn_get_image", "sn_last_error", "sn_destroy"]
+           "sn_get_piece", "sn_get_image", "sn_kernel_name", "sn_last_error", "sn_destroy"]
 
 
 class SnLayer(C.Structure):
@@ -58,13 +58,15 @@ class SnSlabInfo(C.Structure):
     _fields_ = [("image_off", C.c_int64), ("arena_off", C.c_int64), ("bytes", C.c_int64),
                 ("first_piece", C.c_int32), ("n_pieces", C.c_int32),
                 ("t_in_ms", C.c_float), ("t_ex_ms", C.c_float),
-                ("t_in_start_ms", C.c_float), ("t_ex_start_ms", C.c_float)]
+                ("t_in_start_ms", C.c_float), ("t_ex_start_ms", C.c_float),
+                ("wait_slab", C.c_int32)]
 
 
 class SnPieceInfo(C.Structure):
     _fields_ = [("layer", C.c_int32), ("c0", C.c_int32), ("c1", C.c_int32),
                 ("kernel", C.c_int32), ("w_off", C.c_int64), ("b_off", C.c_int64),
-                ("w_bytes", C.c_int64), ("b_bytes", C.c_int64)]
+                ("w_bytes", C.c_int64), ("b_bytes", C.c_int64), ("t_ms", C.c_float),
+                ("ksplit", C.c_int32)]
 
 
 _lib = None
@@ -91,6 +93,7 @@ def load_library(path=LIB_PATH):
         "sn_get_slab": (I, [P, I, C.POINTER(SnSlabInfo)]),
         "sn_get_piece": (I, [P, I, C.POINTER(SnPieceInfo)]),
         "sn_get_image": (I, [P, C.POINTER(C.c_void_p), C.POINTER(C.c_size_t)]),
+        "sn_kernel_name": (C.c_char_p, [I]),
         "sn_last_error": (C.c_char_p, [P]), "sn_destroy": (None, [P]),
     }
     for name, (res, args) in sig.items():
@@ -99,6 +102,10 @@ def load_library(path=LIB_PATH):
         f.argtypes = args
     _lib = lib
     return lib
+
+
+def kernel_name(kernel_id):
+    return load_library().sn_kernel_name(int(kernel_id)).decode()
 
 
 class SwapNetError(RuntimeError):
@@ -296,7 +303,7 @@ def build_engine(net, weights, budget=None, blocks=None, split_budget=None, host
     if max_slab:
         eng.set_option(OPT_MAX_SLAB, max_slab)
     if timing:
-        eng.set_option(OPT_TIMING, 1)
+        eng.set_option(OPT_TIMING, int(timing))
     for a, b in (blocks or net.blocks):
         descs, blob = block_payload(net, weights, a, b)
         eng.add_block(descs, blob)

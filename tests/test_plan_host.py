@@ -76,6 +76,19 @@ def check_plan(net, eng, budget):
             a0, a1 = s["arena_off"], s["arena_off"] + s["bytes"]
             b0, b1 = t["arena_off"], t["arena_off"] + t["bytes"]
             assert a1 <= b0 or b1 <= a0
+        if not st["resident"]:
+            # the swap-in of slab i waits for the compute of slab `wait`; every
+            # slab after that one may still be in use, so none may overlap
+            w = s["wait_slab"]
+            assert w == -1 or 0 <= w <= i - 2
+            for j in range(w + 1, i):
+                t = slabs[j]
+                assert (s["arena_off"] + s["bytes"] <= t["arena_off"] or
+                        t["arena_off"] + t["bytes"] <= s["arena_off"]), (i, j)
+            if w >= 0:
+                t = slabs[w]
+                assert not (s["arena_off"] + s["bytes"] <= t["arena_off"] or
+                            t["arena_off"] + t["bytes"] <= s["arena_off"])
     assert total == st["image_bytes"]
     # streamed bytes: the weights plus alignment padding only
     assert st["image_bytes"] >= net.streamed_weight_bytes()
