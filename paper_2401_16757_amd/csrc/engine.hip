@@ -203,7 +203,7 @@ static void choose_layer_kernels(sn_ctx *c) {
         if (L.d.op != SN_OP_CONV2D) continue;
         const bool is1x1 = L.d.k == 1 && L.d.pad == 0;
         const int M = L.out_h * L.out_w;
-        ConvPlan p = conv_plan(M, L.d.c_out, L.K, is1x1, true);
+        ConvPlan p = conv_plan(M, L.d.c_out, L.K, L.cin_p, is1x1, true);
         L.kernel = p.kernel;
         L.ksplit = p.ksplit;
         L.kps = p.kps;
@@ -435,7 +435,7 @@ static int run_piece(sn_ctx *c, int pi, int n_tok, hipStream_t s) {
             a.relu = (d.flags & SN_FLAG_RELU) ? 1 : 0;
             a.swiglu = swiglu;
             // tile chosen from the whole layer, never from the piece
-            ConvPlan cp = conv_plan(M, (int)L.units * L.rows_per_unit, L.K, true, false);
+            ConvPlan cp = conv_plan(M, (int)L.units * L.rows_per_unit, L.K, L.K, true, false);
             e = launch_conv(cp, a, s);
         }
         break;

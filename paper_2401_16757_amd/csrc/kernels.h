@@ -65,7 +65,7 @@ struct GemvArgs {
     int zero_end;       // if > n0 + units: zero outputs [n0 + units, zero_end)
 };
 
-ConvPlan conv_plan(int M, int N, int K, bool is1x1, bool allow_split);
+ConvPlan conv_plan(int M, int N, int K, int cin_p, bool is1x1, bool allow_split);
 int64_t conv_workspace_bytes(const ConvPlan &p, int M, int N);
 int conv_kernel_count();
 const char *conv_kernel_name(int id);

@@ -19,6 +19,7 @@ namespace sn {
 
 typedef _Float16 h8 __attribute__((ext_vector_type(8)));
 typedef float f16v __attribute__((ext_vector_type(16)));
+typedef float f4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ h8 zero_h8() {
     h8 z;
@@ -42,6 +43,155 @@ __device__ __forceinline__ float silu_f(float v) { return v / (1.0f + expf(-v));
 // and B[k ...][col l%32]; it receives C[8*(v/4) + 4*(l/32) + v%4][l%32] in
 // accumulator register v.
 // ---------------------------------------------------------------------------
+// Epilogue shared by the MFMA conv kernels: either the K-split partial sums
+// (fp32, reduced later in split order) or bias, residual, ReLU / SwiGLU and
+// one rounding to fp16, plus zeros in the output's padding channels.
+template <int BM, int BN, int WM, int WN>
+__device__ __forceinline__ void conv_epilogue(const ConvArgs &a, f16v (&acc)[BM / WM / 32][BN / WN / 32],
+                                              int m0, int nb0, int lane, int wm, int wn) {
+    constexpr int WTM = BM / WM, WTN = BN / WN;
+    constexpr int TM = WTM / 32, TN = WTN / 32;
+    const int lrow = lane & 31;
+    if (a.ksplit > 1) {
+        // partial sums of this K split; splitk_reduce_kernel adds them
+        float *ws = a.ws + (long)blockIdx.y * a.M * a.N;
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+                const int n = nb0 + wn * WTN + j * 32 + lrow;
+#pragma unroll
+                for (int v = 0; v < 16; ++v) {
+                    const int m = m0 + wm * WTM + i * 32 + (v >> 2) * 8 + (lane >> 5) * 4 + (v & 3);
+                    if (m < a.M && n < a.N) ws[(long)m * a.N + n] = acc[i][j][v];
+                }
+            }
+        return;
+    }
+
+    // Epilogue: bias, residual, ReLU / SwiGLU, one rounding to fp16.
+    _Float16 *yg = (_Float16 *)a.y;
+    const _Float16 *bg = (const _Float16 *)a.bias;
+    const _Float16 *rg = (const _Float16 *)a.res;
+    const int units = a.swiglu ? a.N / 2 : a.N;
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+            const int n = nb0 + wn * WTN + j * 32 + lrow;  // weight row (piece-local)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int m = m0 + wm * WTM + i * 32 + (v >> 2) * 8 + (lane >> 5) * 4 + (v & 3);
+                float val = acc[i][j][v];
+                if (a.swiglu) {
+                    // gate (even row) and up (odd row) sit in adjacent lanes
+                    float up = __shfl_xor(val, 1);
+                    if ((n & 1) == 0 && m < a.M && n < a.N) {
+                        float o = silu_f(val) * up;
+                        const long idx = (long)m * a.ldy + a.n0 + (n >> 1);
+                        if (rg) o += (float)rg[idx];
+                        yg[idx] = (_Float16)o;
+                    }
+                    continue;
+                }
+                if (m >= a.M) continue;
+                const long idx = (long)m * a.ldy + a.n0 + n;
+                if (n < a.N) {
+                    if (bg) val += (float)bg[n];
+                    if (rg) val += (float)rg[idx];
+                    if (a.relu) val = fmaxf(val, 0.0f);
+                    yg[idx] = (_Float16)val;
+                } else if (a.n0 + n < a.n_zero_end) {
+                    yg[idx] = (_Float16)0.0f;
+                }
+            }
+        }
+    }
+    (void)units;
+}
+
+
+// Epilogue through LDS for the double-buffered kernel: the fp32 tile is
+// staged in LDS (reusing the operand buffers), then every thread finishes
+// eight consecutive channels of one output pixel with 16-byte bias, residual
+// and output accesses (scalar accesses at ragged edges or when the piece's
+// first channel is not a multiple of 8).  K-split partial sums are written
+// the same way, in fp32.
+template <int BM, int BN, int WM, int WN, int NT>
+__device__ __forceinline__ void conv_epilogue_lds(const ConvArgs &a,
+                                                  f16v (&acc)[BM / WM / 32][BN / WN / 32],
+                                                  float *stage, int m0, int nb0, int lane, int wm,
+                                                  int wn) {
+    constexpr int WTM = BM / WM, WTN = BN / WN;
+    constexpr int TM = WTM / 32, TN = WTN / 32;
+    constexpr int LDS_N = BN + 4;
+    const int lrow = lane & 31;
+    __syncthreads();   // all waves are done reading the operand tiles
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int ml = wm * WTM + i * 32 + (v >> 2) * 8 + (lane >> 5) * 4 + (v & 3);
+                stage[ml * LDS_N + wn * WTN + j * 32 + lrow] = acc[i][j][v];
+            }
+    __syncthreads();
+    const bool vec_ok = (a.n0 % 8) == 0;
+    _Float16 *yg = (_Float16 *)a.y;
+    const _Float16 *bg = (const _Float16 *)a.bias;
+    const _Float16 *rg = (const _Float16 *)a.res;
+    for (int c = threadIdx.x; c < BM * BN / 8; c += NT) {
+        const int ml = c / (BN / 8), nl = (c % (BN / 8)) * 8;
+        const int m = m0 + ml, n = nb0 + nl;
+        if (m >= a.M) continue;
+        float v[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = stage[ml * LDS_N + nl + e];
+        if (a.ksplit > 1) {
+            float *ws = a.ws + (long)blockIdx.y * a.M * a.N + (long)m * a.N;
+            if (n + 8 <= a.N && (a.N % 4) == 0) {
+                *(f4 *)(ws + n) = f4{v[0], v[1], v[2], v[3]};
+                *(f4 *)(ws + n + 4) = f4{v[4], v[5], v[6], v[7]};
+            } else {
+                for (int e = 0; e < 8; ++e)
+                    if (n + e < a.N) ws[n + e] = v[e];
+            }
+            continue;
+        }
+        const long idx = (long)m * a.ldy + a.n0 + n;
+        if (vec_ok && n + 8 <= a.N) {
+            if (bg) {
+                h8 b = *(const h8 *)(bg + n);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) v[e] += (float)b[e];
+            }
+            if (rg) {
+                h8 r = *(const h8 *)(rg + idx);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) v[e] += (float)r[e];
+            }
+            h8 o;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) o[e] = (_Float16)(a.relu ? fmaxf(v[e], 0.0f) : v[e]);
+            *(h8 *)(yg + idx) = o;
+        } else {
+            for (int e = 0; e < 8; ++e) {
+                const int ne = n + e;
+                if (ne < a.N) {
+                    float x = v[e];
+                    if (bg) x += (float)bg[ne];
+                    if (rg) x += (float)rg[idx + e];
+                    if (a.relu) x = fmaxf(x, 0.0f);
+                    yg[idx + e] = (_Float16)x;
+                } else if (a.n0 + ne < a.n_zero_end) {
+                    yg[idx + e] = (_Float16)0.0f;
+                }
+            }
+        }
+    }
+}
+
 template <int BM, int BN, int BK, int WM, int WN, bool IS1X1>
 __global__ __launch_bounds__(WM *WN * 64) void conv_mfma_kernel(ConvArgs a) {
     constexpr int NT = WM * WN * 64;
@@ -160,82 +310,195 @@ __global__ __launch_bounds__(WM *WN * 64) void conv_mfma_kernel(ConvArgs a) {
         }
     }
 
-    if (a.ksplit > 1) {
-        // partial sums of this K split; splitk_reduce_kernel adds them
-        float *ws = a.ws + (long)blockIdx.y * a.M * a.N;
+    conv_epilogue<BM, BN, WM, WN>(a, acc, m0, nb0, lane, wm, wn);
+}
+
+
+// ---------------------------------------------------------------------------
+// Implicit-GEMM convolution, second form: K tile of 64, double-buffered LDS
+// (one barrier per K tile; the global loads of tile t+1 are in flight while
+// tile t is multiplied), and no integer division in the K loop.
+//   MODE 0: 1x1 convolution (any stride, no padding) or token GEMM: the A
+//           row of output pixel m is one contiguous input row.
+//   MODE 1: any kernel size with Cin_p a multiple of 64: a K tile never
+//           crosses a filter tap, so the tap (r, s) and channel offset are
+//           advanced incrementally from tile to tile.
+// Same tile / wave / MFMA layout and epilogue as conv_mfma_kernel.
+// ---------------------------------------------------------------------------
+template <int BM, int BN, int WM, int WN, int MODE>
+__global__ __launch_bounds__(WM *WN * 64) void conv_mfma2_kernel(ConvArgs a) {
+    constexpr int BK = 64;
+    constexpr int NT = WM * WN * 64;
+    constexpr int LDK = BK + 8;
+    constexpr int KC = BK / 8;
+    constexpr int A_CH = BM * KC / NT;
+    constexpr int B_CH = BN * KC / NT;
+    constexpr int WTM = BM / WM, WTN = BN / WN;
+    constexpr int TM = WTM / 32, TN = WTN / 32;
+    static_assert(BM * KC % NT == 0 && BN * KC % NT == 0, "tile/threads mismatch");
+
+    __shared__ __attribute__((aligned(16))) _Float16 lds[2 * (BM + BN) * LDK];
+    _Float16 (*As)[BM * LDK] = (_Float16 (*)[BM * LDK])lds;
+    _Float16 (*Bs)[BN * LDK] = (_Float16 (*)[BN * LDK])(lds + 2 * BM * LDK);
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int wm = wave / WN, wn = wave % WN;
+    const int n_tiles = (a.n_cover + BN - 1) / BN;
+    const int tile_m = blockIdx.x / n_tiles;
+    const int tile_n = blockIdx.x % n_tiles;
+    const int m0 = tile_m * BM, nb0 = tile_n * BN;
+    const int kc = tid % KC;
+    const int row_base = tid / KC;
+    constexpr int ROW_STEP = NT / KC;
+
+    const _Float16 *xg = (const _Float16 *)a.x;
+    const _Float16 *wg = (const _Float16 *)a.w;
+
+    // per A row: input pixel origin (MODE 1) or row pointer (MODE 0)
+    int a_iy0[A_CH], a_ix0[A_CH];
+    bool a_ok[A_CH];
 #pragma unroll
-        for (int i = 0; i < TM; ++i)
+    for (int i = 0; i < A_CH; ++i) {
+        int m = m0 + row_base + i * ROW_STEP;
+        a_ok[i] = m < a.M;
+        int oy = a_ok[i] ? m / a.Wo : 0;
+        int ox = a_ok[i] ? m - oy * a.Wo : 0;
+        a_iy0[i] = oy * a.stride - a.pad;
+        a_ix0[i] = ox * a.stride - a.pad;
+    }
+    bool b_ok[B_CH];
+    const _Float16 *b_row[B_CH];
 #pragma unroll
-            for (int j = 0; j < TN; ++j) {
-                const int n = nb0 + wn * WTN + j * 32 + lrow;
-#pragma unroll
-                for (int v = 0; v < 16; ++v) {
-                    const int m = m0 + wm * WTM + i * 32 + (v >> 2) * 8 + (lane >> 5) * 4 + (v & 3);
-                    if (m < a.M && n < a.N) ws[(long)m * a.N + n] = acc[i][j][v];
-                }
-            }
-        return;
+    for (int i = 0; i < B_CH; ++i) {
+        int n = nb0 + row_base + i * ROW_STEP;
+        b_ok[i] = n < a.N;
+        b_row[i] = wg + (long)(b_ok[i] ? n : 0) * a.K + kc * 8;
     }
 
-    // Epilogue: bias, residual, ReLU / SwiGLU, one rounding to fp16.
-    _Float16 *yg = (_Float16 *)a.y;
-    const _Float16 *bg = (const _Float16 *)a.bias;
-    const _Float16 *rg = (const _Float16 *)a.res;
-    const int units = a.swiglu ? a.N / 2 : a.N;
+    const int kbeg = blockIdx.y * a.kps;
+    const int kend = min(a.K, kbeg + a.kps);
+    // filter tap and channel offset of the current K tile (MODE 1)
+    int tap_r = 0, tap_s = 0, ci0 = kbeg;
+    if (MODE == 1) {
+        int rs = kbeg / a.Cin_p;
+        ci0 = kbeg - rs * a.Cin_p;
+        tap_r = rs / a.kw;
+        tap_s = rs - tap_r * a.kw;
+    }
+
+    h8 ra[A_CH], rb[B_CH];
+    auto load_tile = [&](int k0) {
+        const int k = k0 + kc * 8;
+        const bool kok = k < kend;
 #pragma unroll
-    for (int i = 0; i < TM; ++i) {
+        for (int i = 0; i < A_CH; ++i) {
+            if (MODE == 0) {
+                bool ok = kok && a_ok[i];
+                ra[i] = ok ? *(const h8 *)(xg + ((long)a_iy0[i] * a.W + a_ix0[i]) * a.Cin_p + k)
+                           : zero_h8();
+            } else {
+                int iy = a_iy0[i] + tap_r * a.dil;
+                int ix = a_ix0[i] + tap_s * a.dil;
+                bool ok = kok && a_ok[i] && iy >= 0 && iy < a.H && ix >= 0 && ix < a.W;
+                ra[i] = ok ? *(const h8 *)(xg + ((long)iy * a.W + ix) * a.Cin_p + ci0 + kc * 8)
+                           : zero_h8();
+            }
+        }
 #pragma unroll
-        for (int j = 0; j < TN; ++j) {
-            const int n = nb0 + wn * WTN + j * 32 + lrow;  // weight row (piece-local)
-#pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const int m = m0 + wm * WTM + i * 32 + (v >> 2) * 8 + (lane >> 5) * 4 + (v & 3);
-                float val = acc[i][j][v];
-                if (a.swiglu) {
-                    // gate (even row) and up (odd row) sit in adjacent lanes
-                    float up = __shfl_xor(val, 1);
-                    if ((n & 1) == 0 && m < a.M && n < a.N) {
-                        float o = silu_f(val) * up;
-                        const long idx = (long)m * a.ldy + a.n0 + (n >> 1);
-                        if (rg) o += (float)rg[idx];
-                        yg[idx] = (_Float16)o;
-                    }
-                    continue;
-                }
-                if (m >= a.M) continue;
-                const long idx = (long)m * a.ldy + a.n0 + n;
-                if (n < a.N) {
-                    if (bg) val += (float)bg[n];
-                    if (rg) val += (float)rg[idx];
-                    if (a.relu) val = fmaxf(val, 0.0f);
-                    yg[idx] = (_Float16)val;
-                } else if (a.n0 + n < a.n_zero_end) {
-                    yg[idx] = (_Float16)0.0f;
+        for (int i = 0; i < B_CH; ++i)
+            rb[i] = (kok && b_ok[i]) ? *(const h8 *)(b_row[i] + k0) : zero_h8();
+        if (MODE == 1) {
+            ci0 += BK;
+            if (ci0 >= a.Cin_p) {
+                ci0 = 0;
+                if (++tap_s == a.kw) {
+                    tap_s = 0;
+                    ++tap_r;
                 }
             }
         }
+    };
+    auto store_tile = [&](int buf) {
+#pragma unroll
+        for (int i = 0; i < A_CH; ++i)
+            *(h8 *)(&As[buf][(row_base + i * ROW_STEP) * LDK + kc * 8]) = ra[i];
+#pragma unroll
+        for (int i = 0; i < B_CH; ++i)
+            *(h8 *)(&Bs[buf][(row_base + i * ROW_STEP) * LDK + kc * 8]) = rb[i];
+    };
+
+    f16v acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
+
+    const int lrow = lane & 31;
+    const int lk = (lane >> 5) * 8;
+
+    load_tile(kbeg);
+    store_tile(0);
+    __syncthreads();
+    int cur = 0;
+    for (int k0 = kbeg; k0 < kend; k0 += BK) {
+        const bool more = k0 + BK < kend;
+        if (more) load_tile(k0 + BK);
+#pragma unroll
+        for (int kk = 0; kk < BK; kk += 16) {
+            h8 fa[TM], fb[TN];
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+                fa[i] = *(const h8 *)(&As[cur][(wm * WTM + i * 32 + lrow) * LDK + kk + lk]);
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+                fb[j] = *(const h8 *)(&Bs[cur][(wn * WTN + j * 32 + lrow) * LDK + kk + lk]);
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fa[i], fb[j], acc[i][j],
+                                                                        0, 0, 0);
+        }
+        if (more) store_tile(cur ^ 1);
+        __syncthreads();
+        cur ^= 1;
     }
-    (void)units;
+    static_assert(BM * (BN + 4) * 4 <= 2 * (BM + BN) * LDK * 2, "staging tile exceeds LDS");
+    if (a.swiglu)
+        conv_epilogue<BM, BN, WM, WN>(a, acc, m0, nb0, lane, wm, wn);
+    else
+        conv_epilogue_lds<BM, BN, WM, WN, NT>(a, acc, (float *)lds, m0, nb0, lane, wm, wn);
 }
 
 struct ConvVariant {
     int bm, bn, bk;
-    bool is1x1;
+    int kind;   // 0: conv_mfma general, 1: conv_mfma 1x1, 2: conv_mfma2 1x1, 3: conv_mfma2 aligned
     const char *name;
     void (*fn)(ConvArgs);
     int threads;
 };
 
 #define SN_CONV_VARIANT(BM, BN, BK, WM, WN, ONE, SUFFIX)                          \
-    {BM, BN, BK, ONE, "conv_mfma_" #BM "x" #BN "x" #BK "_w" #WM #WN SUFFIX, \
+    {BM, BN, BK, ONE ? 1 : 0, "conv_mfma_" #BM "x" #BN "x" #BK "_w" #WM #WN SUFFIX, \
      conv_mfma_kernel<BM, BN, BK, WM, WN, ONE>, WM * WN * 64}
 #define SN_CONV_PAIR(BM, BN, BK, WM, WN) \
     SN_CONV_VARIANT(BM, BN, BK, WM, WN, false, "_gen"), SN_CONV_VARIANT(BM, BN, BK, WM, WN, true, "_1x1")
+#define SN_CONV2_PAIR(BM, BN, WM, WN)                                                        \
+    {BM, BN, 64, 2, "conv2_mfma_" #BM "x" #BN "_w" #WM #WN "_1x1", conv_mfma2_kernel<BM, BN, WM, WN, 0>, \
+     WM * WN * 64},                                                                            \
+    {BM, BN, 64, 3, "conv2_mfma_" #BM "x" #BN "_w" #WM #WN "_tap", conv_mfma2_kernel<BM, BN, WM, WN, 1>, \
+     WM * WN * 64}
 
 static const ConvVariant kConvVariants[] = {
     SN_CONV_PAIR(128, 128, 32, 2, 2), SN_CONV_PAIR(128, 64, 32, 2, 2),
     SN_CONV_PAIR(64, 128, 32, 2, 2),  SN_CONV_PAIR(64, 64, 32, 2, 2),
     SN_CONV_PAIR(32, 64, 64, 1, 2),   SN_CONV_PAIR(32, 32, 64, 1, 1),
+    SN_CONV2_PAIR(128, 128, 2, 2),    SN_CONV2_PAIR(128, 64, 2, 2),
+    SN_CONV2_PAIR(64, 128, 2, 2),     SN_CONV2_PAIR(64, 64, 2, 2),
 };
 static constexpr int kNumConvVariants = sizeof(kConvVariants) / sizeof(kConvVariants[0]);
 
@@ -260,18 +523,26 @@ __global__ void splitk_reduce_kernel(ConvArgs a) {
     }
     const long plane = (long)a.M * a.N;
     const float *p = a.ws + (long)m * a.N + n;
+    // loads issued eight at a time, added strictly in split order
     float v = 0.0f;
-    for (int s = 0; s < a.ksplit; ++s) v += p[s * plane];
+    int s = 0;
+    for (; s + 8 <= a.ksplit; s += 8) {
+        float q[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) q[e] = p[(long)(s + e) * plane];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v += q[e];
+    }
+    for (; s < a.ksplit; ++s) v += p[(long)s * plane];
     if (a.bias) v += (float)((const _Float16 *)a.bias)[n];
     if (a.res) v += (float)((const _Float16 *)a.res)[idx];
     if (a.relu) v = fmaxf(v, 0.0f);
     yg[idx] = (_Float16)v;
 }
 
-static int find_variant(int bm, int bn, bool is1x1) {
+static int find_variant(int bm, int bn, int kind) {
     for (int id = 0; id < kNumConvVariants; ++id)
-        if (kConvVariants[id].bm == bm && kConvVariants[id].bn == bn &&
-            kConvVariants[id].is1x1 == is1x1)
+        if (kConvVariants[id].bm == bm && kConvVariants[id].bn == bn && kConvVariants[id].kind == kind)
             return id;
     return -1;
 }
@@ -279,24 +550,28 @@ static int find_variant(int bm, int bn, bool is1x1) {
 // Tile and K split from the whole layer's shape (never from a slab's channel
 // range): the largest 4-wave tile that gives every CU a block; otherwise
 // 64 x 64 tiles with the K range split so that about 256 blocks run, each
-// over at least four K tiles.
-ConvPlan conv_plan(int M, int N, int K, bool is1x1, bool allow_split) {
+// over at least four K tiles of 32 (two of 64).  1x1 convolutions and taps
+// with Cin_p a multiple of 64 use the double-buffered kernel; the rest (the
+// first layers, Cin_p < 64) the single-buffered one.
+ConvPlan conv_plan(int M, int N, int K, int cin_p, bool is1x1, bool allow_split) {
     const int target = 256;
+    const int kind = is1x1 ? 2 : (cin_p % 64 == 0 ? 3 : 0);
     ConvPlan p;
     static const int tiles[][2] = {{128, 128}, {128, 64}, {64, 128}, {64, 64}};
     for (auto &t : tiles) {
         long blocks = (long)((M + t[0] - 1) / t[0]) * ((N + t[1] - 1) / t[1]);
         if (blocks >= target - 16) {
-            p.kernel = find_variant(t[0], t[1], is1x1);
+            p.kernel = find_variant(t[0], t[1], kind);
             p.kps = K;
             return p;
         }
     }
-    p.kernel = find_variant(64, 64, is1x1);
+    p.kernel = find_variant(64, 64, kind);
     const ConvVariant &v = kConvVariants[p.kernel];
     long blocks = (long)((M + 63) / 64) * ((N + 63) / 64);
     const int kt = (K + v.bk - 1) / v.bk;
-    int s = allow_split ? (int)std::min<long>((target + blocks - 1) / blocks, kt / 4) : 1;
+    const int min_tiles = v.bk == 64 ? 2 : 4;
+    int s = allow_split ? (int)std::min<long>((target + blocks - 1) / blocks, kt / min_tiles) : 1;
     if (s < 2) {
         p.kps = K;
         return p;
