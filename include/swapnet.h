@@ -157,13 +157,19 @@ enum sn_option {
                                    (adds launch overhead; for profiling only).
                                    May be set after plan                      */
     SN_OPT_MAX_SLAB = 3,        /* cap on slab bytes (0 = none)               */
-    SN_OPT_SWAPIN = 5,          /* how a slab is swapped in: 0 (default) a copy
-                                   kernel on the copy stream reads the pinned
-                                   image through its device mapping (ordering
-                                   by stream barriers, no host round trip);
-                                   1: hipMemcpyAsync (SDMA engine)            */
+    SN_OPT_SWAPIN = 5,          /* how a slab is swapped in.  2 (default):
+                                   hipMemcpyAsync (SDMA engine) issued by the
+                                   context's copy thread once the compute it
+                                   must follow has finished, so the calling
+                                   thread never blocks; 1: the same DMA issued
+                                   by the calling thread with a stream-event
+                                   dependency (the runtime then blocks the
+                                   caller until the dependency is met); 0: a
+                                   copy kernel on the copy stream reads the
+                                   pinned image through its device mapping
+                                   (uses compute units, never blocks)         */
     SN_OPT_SWAPIN_BLOCKS = 6,   /* workgroups of the swap-in copy kernel
-                                   (default 128)                              */
+                                   (default 32)                               */
     SN_OPT_GRAPH = 4            /* 1 (default): the kernels of each slab of an
                                    image network are captured once per
                                    (input, output) buffer pair into one HIP

@@ -14,8 +14,13 @@
 //             back, the range is simply reused.
 #include <hip/hip_runtime.h>
 
+#include <atomic>
 #include <chrono>
+#include <condition_variable>
 #include <cstdio>
+#include <memory>
+#include <mutex>
+#include <thread>
 #include <cstdlib>
 #include <cstring>
 #include <string>
@@ -50,8 +55,21 @@ struct sn_ctx {
     hipStream_t copy_s = nullptr, comp_s = nullptr;
     uint8_t *image = nullptr;          // pinned (device mode) or malloc (host-only)
     uint8_t *image_dev = nullptr;      // the pinned image as seen from the device
-    int swapin = 0;                    // 0: copy kernel on the copy stream, 1: SDMA
-    int swapin_blocks = 128;
+    int swapin = 2;                    // see SN_OPT_SWAPIN
+    int swapin_blocks = 32;
+    // copy thread (SN_OPT_SWAPIN = 2): issues the swap-in DMAs of inference
+    // `seq` in slab order, each once the compute it must follow has finished
+    std::thread copier;
+    std::mutex mu;
+    std::condition_variable cv;
+    uint64_t requested = 0;            // guarded by mu
+    bool stop = false;                 // guarded by mu
+    uint64_t seq = 0;                  // inference sequence number (main thread)
+    std::atomic<uint64_t> handled{0};  // last inference whose copies were all issued
+    std::atomic<uint64_t> fork_seq{0}, abort_seq{0};
+    std::unique_ptr<std::atomic<uint64_t>[]> done_seq, loaded_seq;
+    std::atomic<int> copy_error{0};
+    std::string copy_err;
     uint8_t *act = nullptr;
     int64_t act_bytes = 0;
     uint8_t *kv = nullptr;
@@ -85,6 +103,9 @@ struct sn_ctx {
 };
 
 static thread_local std::string g_create_err;
+static void wait_copier_idle(sn_ctx *c);
+static void start_copier(sn_ctx *c);
+static void stop_copier(sn_ctx *c);
 
 static int fail(sn_ctx *c, int code, const std::string &msg) {
     if (c) c->err = msg;
@@ -178,7 +199,8 @@ extern "C" int sn_set_option(sn_ctx *c, int option, int64_t value) {
         c->timing = (int)value;
         return SN_OK;
     case SN_OPT_SWAPIN:
-        if (value < 0 || value > 1) return fail(c, SN_E_INVALID, "swap-in mode must be 0 or 1");
+        if (value < 0 || value > 2) return fail(c, SN_E_INVALID, "swap-in mode must be 0, 1 or 2");
+        if (c->state == ST_PLANNED && c->have_prev) wait_copier_idle(c);
         c->swapin = (int)value;
         return SN_OK;
     case SN_OPT_SWAPIN_BLOCKS:
@@ -335,6 +357,7 @@ extern "C" int sn_plan(sn_ctx *c) {
     c->slab_t_in_start.assign(ns, 0.f);
     c->slab_t_ex_start.assign(ns, 0.f);
 
+    if (!c->plan.resident) start_copier(c);
     if (c->plan.resident) {
         // everything fits: one upload now, no swapping per inference
         for (const Slab &s : c->plan.slabs)
@@ -473,6 +496,89 @@ static int run_piece(sn_ctx *c, int pi, int n_tok, hipStream_t s) {
     return SN_OK;
 }
 
+// ---------------------------------------------------------------------------
+// Copy thread.  A DMA on the SDMA engine that must wait for a compute event
+// makes hipMemcpyAsync block the calling thread until the event fires, so
+// the main thread could not queue work ahead.  The copy thread takes that
+// wait instead: for slab i of inference `seq` it waits until the main thread
+// has recorded the event the slab must follow (fork, or done[wait]) for this
+// inference, polls it to completion, issues the DMA (no device-side
+// dependency left) and records loaded[i].  The main thread makes the
+// compute stream wait on loaded[i] once the copy thread has recorded it.
+// ---------------------------------------------------------------------------
+static inline void cpu_relax() { __builtin_ia32_pause(); }
+
+static void copier_main(sn_ctx *c) {
+    const int ns = (int)c->plan.slabs.size();
+    for (;;) {
+        uint64_t seq;
+        {
+            std::unique_lock<std::mutex> lk(c->mu);
+            c->cv.wait(lk, [&] { return c->stop || c->requested > c->handled.load(); });
+            if (c->stop) return;
+            seq = c->handled.load() + 1;
+        }
+        bool aborted = false;
+        for (int i = 0; i < ns && !aborted; ++i) {
+            const Slab &s = c->plan.slabs[i];
+            std::atomic<uint64_t> &gate = s.wait >= 0 ? c->done_seq[s.wait] : c->fork_seq;
+            hipEvent_t ev = s.wait >= 0 ? c->done[s.wait] : c->fork;
+            while (gate.load(std::memory_order_acquire) < seq) {
+                if (c->abort_seq.load() >= seq) {
+                    aborted = true;
+                    break;
+                }
+                cpu_relax();
+            }
+            if (aborted) break;
+            hipError_t e;
+            while ((e = hipEventQuery(ev)) == hipErrorNotReady) {
+                for (int k = 0; k < 64; ++k) cpu_relax();
+            }
+            if (e == hipSuccess && c->timing) e = hipEventRecord(c->t_in0[i], c->copy_s);
+            if (e == hipSuccess && s.bytes)
+                e = hipMemcpyAsync(c->arena + s.arena_off, c->image + s.image_off, (size_t)s.bytes,
+                                   hipMemcpyHostToDevice, c->copy_s);
+            if (e == hipSuccess && c->timing) e = hipEventRecord(c->t_in1[i], c->copy_s);
+            if (e == hipSuccess) e = hipEventRecord(c->loaded[i], c->copy_s);
+            if (e != hipSuccess && !c->copy_error.load()) {
+                c->copy_err = std::string("swap-in DMA: ") + hipGetErrorString(e);
+                c->copy_error.store(1);
+            }
+            c->loaded_seq[i].store(seq, std::memory_order_release);
+        }
+        if (aborted)
+            for (int i = 0; i < ns; ++i) c->loaded_seq[i].store(seq, std::memory_order_release);
+        c->handled.store(seq);
+    }
+}
+
+static void wait_copier_idle(sn_ctx *c) {
+    if (!c->copier.joinable()) return;
+    while (c->handled.load() < c->seq) cpu_relax();
+}
+
+static void start_copier(sn_ctx *c) {
+    const int ns = (int)c->plan.slabs.size();
+    c->done_seq.reset(new std::atomic<uint64_t>[ns]);
+    c->loaded_seq.reset(new std::atomic<uint64_t>[ns]);
+    for (int i = 0; i < ns; ++i) {
+        c->done_seq[i].store(0);
+        c->loaded_seq[i].store(0);
+    }
+    c->copier = std::thread(copier_main, c);
+}
+
+static void stop_copier(sn_ctx *c) {
+    if (!c->copier.joinable()) return;
+    {
+        std::lock_guard<std::mutex> lk(c->mu);
+        c->stop = true;
+    }
+    c->cv.notify_all();
+    c->copier.join();
+}
+
 // Swap-in of slab i on the copy stream.  It overwrites arena bytes last used
 // by slab `wait` (the newest earlier slab overlapping its range), so it waits
 // for that slab's compute; a slab with no such predecessor waits only for
@@ -482,7 +588,7 @@ static int enqueue_copy(sn_ctx *c, int i) {
     HIP_TRY(c, hipStreamWaitEvent(c->copy_s, s.wait >= 0 ? c->done[s.wait] : c->fork, 0));
     if (c->timing) HIP_TRY(c, hipEventRecord(c->t_in0[i], c->copy_s));
     if (s.bytes) {
-        if (c->swapin == 1)
+        if (c->swapin != 0)
             HIP_TRY(c, hipMemcpyAsync(c->arena + s.arena_off, c->image + s.image_off,
                                       (size_t)s.bytes, hipMemcpyHostToDevice, c->copy_s));
         else
@@ -513,33 +619,65 @@ template <typename Pre, typename Post>
 static int run_slabs(sn_ctx *c, int n_tok, hipStream_t cs, Pre pre, Post post, bool graphs) {
     const int ns = (int)c->plan.slabs.size();
     const bool swap = !c->plan.resident;
+    const bool threaded = swap && c->swapin == 2;
     int rc;
+    uint64_t seq = 0;
+    if (threaded) {
+        // the copy thread must be done with the previous inference's events
+        // before they are recorded again
+        wait_copier_idle(c);
+        if (c->copy_error.exchange(0)) return fail(c, SN_E_HIP, c->copy_err);
+        seq = ++c->seq;
+    }
+    auto abort_copies = [&](int r) {
+        if (threaded) c->abort_seq.store(seq);
+        return r;
+    };
     if (c->timing) HIP_TRY(c, hipEventRecord(c->t_start, cs));
-    HIP_TRY(c, hipEventRecord(c->fork, cs));
+    if (hipError_t e = hipEventRecord(c->fork, cs))
+        return abort_copies(fail(c, SN_E_HIP, std::string("fork: ") + hipGetErrorString(e)));
     // copies are issued in slab order, each as soon as the compute it waits
-    // for has been enqueued
+    // for has been enqueued (calling thread) or has finished (copy thread)
     int next_copy = 0;
     auto issue = [&](int done_upto) -> int {
-        while (swap && next_copy < ns && c->plan.slabs[next_copy].wait <= done_upto) {
+        while (swap && !threaded && next_copy < ns && c->plan.slabs[next_copy].wait <= done_upto) {
             int r = enqueue_copy(c, next_copy++);
             if (r) return r;
         }
         return SN_OK;
     };
-    if ((rc = issue(-1))) return rc;
-    for (int i = 0; i < ns; ++i) {
-        if (swap) HIP_TRY(c, hipStreamWaitEvent(cs, c->loaded[i], 0));
-        if (c->timing) HIP_TRY(c, hipEventRecord(c->t_ex0[i], cs));
-        if (graphs) {
-            HIP_TRY(c, hipGraphLaunch(c->graphs[i], cs));
-        } else {
-            if (i == 0 && (rc = pre(cs))) return rc;
-            if ((rc = slab_kernels(c, i, n_tok, cs))) return rc;
-            if (i == ns - 1 && (rc = post(cs))) return rc;
+    if (threaded) {
+        c->fork_seq.store(seq, std::memory_order_release);
+        {
+            std::lock_guard<std::mutex> lk(c->mu);
+            c->requested = seq;
         }
-        if (c->timing) HIP_TRY(c, hipEventRecord(c->t_ex1[i], cs));
-        HIP_TRY(c, hipEventRecord(c->done[i], cs));
-        if ((rc = issue(i))) return rc;
+        c->cv.notify_one();
+    } else if ((rc = issue(-1))) {
+        return rc;
+    }
+    for (int i = 0; i < ns; ++i) {
+        if (threaded) {
+            while (c->loaded_seq[i].load(std::memory_order_acquire) < seq) cpu_relax();
+            if (c->copy_error.load()) return abort_copies(fail(c, SN_E_HIP, c->copy_err));
+        }
+        hipError_t e = hipSuccess;
+        if (swap) e = hipStreamWaitEvent(cs, c->loaded[i], 0);
+        if (e == hipSuccess && c->timing) e = hipEventRecord(c->t_ex0[i], cs);
+        if (e != hipSuccess) return abort_copies(fail(c, SN_E_HIP, hipGetErrorString(e)));
+        if (graphs) {
+            if ((e = hipGraphLaunch(c->graphs[i], cs)) != hipSuccess)
+                return abort_copies(fail(c, SN_E_HIP, std::string("graph launch: ") + hipGetErrorString(e)));
+        } else {
+            if (i == 0 && (rc = pre(cs))) return abort_copies(rc);
+            if ((rc = slab_kernels(c, i, n_tok, cs))) return abort_copies(rc);
+            if (i == ns - 1 && (rc = post(cs))) return abort_copies(rc);
+        }
+        if (c->timing) e = hipEventRecord(c->t_ex1[i], cs);
+        if (e == hipSuccess) e = hipEventRecord(c->done[i], cs);
+        if (e != hipSuccess) return abort_copies(fail(c, SN_E_HIP, hipGetErrorString(e)));
+        if (threaded) c->done_seq[i].store(seq, std::memory_order_release);
+        else if ((rc = issue(i))) return rc;
     }
     return SN_OK;
 }
@@ -808,6 +946,7 @@ extern "C" const char *sn_last_error(const sn_ctx *c) {
 
 extern "C" void sn_destroy(sn_ctx *c) {
     if (!c) return;
+    stop_copier(c);
     if (!c->host_only) {
         if (c->comp_s) hipStreamSynchronize(c->comp_s);
         if (c->copy_s) hipStreamSynchronize(c->copy_s);
