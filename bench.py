@@ -38,7 +38,9 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="resnet50",
-                    choices=["tiny_cnn", "resnet50", "vgg16", "fcn_resnet101"])
+                    choices=["tiny_cnn", "resnet50", "vgg16", "fcn_resnet101", "decoder7b"])
+    ap.add_argument("--gen-tokens", type=int, default=None,
+                    help="decoder: tokens generated after the prompt (default 128)")
     ap.add_argument("--budget-frac", type=float, default=None,
                     help="budget as a fraction of the weight bytes (default: the workload's)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
@@ -46,6 +48,10 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--verbose", action="store_true")
     ap.add_argument("--no-graph", action="store_true", help="enqueue call by call (no HIP graph)")
+    ap.add_argument("--swapin", type=int, default=2, choices=[0, 1, 2],
+                    help="0 copy kernel, 1 SDMA from the calling thread, 2 SDMA from the copy thread")
+    ap.add_argument("--pmc-calibration", action="store_true",
+                    help="also run one 256 MiB device-to-device copy (counter calibration)")
     return ap.parse_args()
 
 
@@ -129,8 +135,10 @@ def conv_flops(spec, c0, c1):
 
 
 def kernel_profile(S, net, eng, torch, xd, yd):
-    """Per-piece kernel times of one inference (timing level 2), grouped by
-    kernel.  Returns {name: (launches, total_ms, flops, bytes)}."""
+    """Per-kernel times of one inference (timing level 2: a HIP event pair
+    around every layer piece, plus one between a split-K convolution's main
+    kernel and its reduction), grouped by kernel.
+    Returns {name: [launches, total_ms, flops, bytes]}."""
     s = torch.cuda.current_stream()
     eng.set_option(S.OPT_TIMING, 2)
     for _ in range(2):
@@ -141,24 +149,28 @@ def kernel_profile(S, net, eng, torch, xd, yd):
     eng.infer(x)
     eng.set_option(S.OPT_TIMING, 0)
     groups = {}
+
+    def add(name, t, fl, by):
+        g = groups.setdefault(name, [0, 0.0, 0.0, 0.0])
+        g[0] += 1
+        g[1] += t
+        g[2] += fl
+        g[3] += by
     for p in eng.pieces():
         spec = net.layers[p["layer"]]
         if spec.op == "conv2d":
-            name = S.kernel_name(p["kernel"])
-            fl = conv_flops(spec, p["c0"], p["c1"])
-            by = p["w_bytes"] + p["b_bytes"]
+            ho, wo = spec.out_hw()
+            m, n = ho * wo, p["c1"] - p["c0"]
+            add(S.kernel_name(p["kernel"]), p["t_main_ms"], conv_flops(spec, p["c0"], p["c1"]),
+                p["w_bytes"] + p["b_bytes"])
+            if p["ksplit"] > 1:
+                add("splitk_reduce", p["t_ms"] - p["t_main_ms"], 0.0,
+                    4.0 * p["ksplit"] * m * n + 2.0 * m * n)
         elif spec.op == "linear":
-            name = "gemv"
-            fl = 2.0 * (p["c1"] - p["c0"]) * spec.c_in
-            by = p["w_bytes"] + p["b_bytes"] + 2 * spec.c_in + 2 * (p["c1"] - p["c0"])
+            add("gemv", p["t_ms"], 2.0 * (p["c1"] - p["c0"]) * spec.c_in,
+                p["w_bytes"] + p["b_bytes"] + 2 * spec.c_in + 2 * (p["c1"] - p["c0"]))
         else:
-            name = spec.op
-            fl, by = 0.0, 0.0
-        g = groups.setdefault(name, [0, 0.0, 0.0, 0.0])
-        g[0] += 1
-        g[1] += p["t_ms"]
-        g[2] += fl
-        g[3] += by
+            add(spec.op, p["t_ms"], 0.0, 0.0)
     return groups
 
 
@@ -205,6 +217,85 @@ def cpu_baseline(net, wts, x, seconds):
                       % (n, net.name, el)}
 
 
+
+def build_decoder(S, W, net, budget):
+    """Register the decoder block by block, generating each block's weights
+    just before it is added (the 13.5 GB of fp16 weights never coexist with
+    a second full copy on the Python side)."""
+    eng = S.SwapNet(budget)
+    for a_, b_ in net.blocks:
+        params = W.layers_params(net, range(a_, b_))
+        descs, blob = S.block_payload(net, lambda li: params[li], a_, b_)
+        eng.add_block(descs, blob)
+        del params, blob
+    eng.plan()
+    eng.out_shape, eng.out_dtype = S.output_shape(net)
+    return eng
+
+
+def run_decoder(eng, prompt, gen):
+    """Greedy generation: prefill, then gen-1 single-token steps.  Returns
+    (prefill_ms, per-step ms list, token ids)."""
+    eng.reset()
+    t0 = time.perf_counter()
+    logits = eng.infer_tokens(prompt)
+    pre = (time.perf_counter() - t0) * 1e3
+    steps, ids = [], []
+    for _ in range(gen - 1):
+        nxt = int(np.argmax(logits))
+        ids.append(nxt)
+        t0 = time.perf_counter()
+        logits = eng.infer_tokens(np.array([nxt], np.int32))
+        steps.append((time.perf_counter() - t0) * 1e3)
+    return pre, steps, ids
+
+
+def bench_decoder(a, torch, S, W):
+    net = W.get_network("decoder7b")
+    gen = a.gen_tokens or net.extra["gen"]
+    prompt = W.make_input(net)
+    budget = net.budget_bytes()
+    log("building swapped decoder (budget %d B = 4 layers)" % budget)
+    eng = build_decoder(S, W, net, budget)
+    st = eng.stats()
+    log("timing prefill + %d decode steps (swapped)" % (gen - 1))
+    run_decoder(eng, prompt[:8], 3)                      # warm-up
+    pre, steps, ids = run_decoder(eng, prompt, gen)
+    eng.close()
+    log("building resident decoder")
+    eng_r = build_decoder(S, W, net, st["image_bytes"] + (1 << 20))
+    run_decoder(eng_r, prompt[:8], 3)
+    pre_r, steps_r, ids_r = run_decoder(eng_r, prompt, gen)
+    eng_r.close()
+    peak = measure_h2d_peak(torch)
+    dec = float(np.median(steps))
+    dec_r = float(np.median(steps_r))
+    streamed = st["streamed_bytes"] + 2 * net.extra["d"]   # + one embedding row
+    out = {
+        "metric": METRIC, "value": round(dec / dec_r, 3), "unit": "x (swapped/resident decode latency)",
+        "n_gpus": 1, "steps": gen - 1, "warmup": 2, "ms_per_step": round(dec, 3),
+        "higher_is_better": False, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f16 (fp32 accumulate)", "data": "synthetic (seeded N(0,0.02) weights, random prompt)",
+        "config": {"workload": "decoder7b", "batch": 1, "prompt": len(prompt), "generated": gen,
+                   "weight_bytes": net.weight_bytes(), "budget_bytes": budget,
+                   "budget_fraction": "4 layers", "slabs": st["n_slabs"],
+                   "parallelism": "none (1 GPU)"},
+        "prefill_ms": round(pre, 2), "resident_prefill_ms": round(pre_r, 2),
+        "decode_ms_per_token": round(dec, 3), "resident_decode_ms_per_token": round(dec_r, 3),
+        "decode_tokens_per_s": round(1e3 / dec, 3),
+        "streamed_bytes_per_token": streamed,
+        "h2d_gbps": round(streamed / (dec * 1e-3) / 1e9, 2), "h2d_peak_gbps": round(peak, 2),
+        "h2d_frac": round(streamed / (dec * 1e-3) / 1e9 / peak, 4),
+        "link": {"bound": "pcie_h2d", "achieved": round(streamed / (dec * 1e-3) / 1e9, 2),
+                 "peak": round(peak, 2), "unit": "GB/s",
+                 "frac": round(streamed / (dec * 1e-3) / 1e9 / peak, 4), "traffic": streamed},
+        "resident_hbm_gbps": round(streamed / (dec_r * 1e-3) / 1e9, 1),
+        "same_tokens_swapped_and_resident": ids == ids_r,
+        "kv_bytes": st["kv_bytes"], "swapin_mode": "SDMA, copy thread",
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     a = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -222,6 +313,8 @@ def main():
     # (recorded on the current stream) bracket it
     stream = torch.cuda.Stream()
     torch.cuda.set_stream(stream)
+    if a.workload == "decoder7b":
+        return bench_decoder(a, torch, S, W)
     net = W.get_network(a.workload)
     log("generating %s weights" % net.name)
     wts = W.make_weights(net)
@@ -234,6 +327,7 @@ def main():
     eng_sw = S.build_engine(net, wts, budget=budget)
     st = eng_sw.stats()
     eng_res = S.build_engine(net, wts, budget=st["image_bytes"] + 4096)
+    eng_sw.set_option(S.OPT_SWAPIN, a.swapin)
     if a.no_graph:
         eng_sw.set_option(S.OPT_GRAPH, 0)
         eng_res.set_option(S.OPT_GRAPH, 0)
@@ -245,6 +339,14 @@ def main():
 
     log("measuring pinned H2D peak")
     peak = measure_h2d_peak(torch)
+    if a.pmc_calibration:
+        src = torch.empty(256 << 20, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        src.fill_(3)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     log("timing %d swapped steps" % a.steps)
     sw_ms, sw_wall = timed_loop(torch, eng_sw, xd, yd, a.steps, a.warmup)
@@ -262,7 +364,7 @@ def main():
     log("timeline and kernel profile (untimed passes)")
     tl = slab_timeline(S, eng_sw, x)
     groups = kernel_profile(S, net, eng_res, torch, xd, yr)
-    conv = {k: v for k, v in groups.items() if k.startswith("conv_mfma")}
+    conv = {k: v for k, v in groups.items() if k.startswith("conv")}
     dom = max(conv.items(), key=lambda kv: kv[1][1]) if conv else None
     total_flops = sum(v[2] for v in groups.values())
     res_compute_ms = sum(v[1] for v in groups.values())
@@ -311,6 +413,7 @@ def main():
         "swapped_equals_resident_bitwise": bitwise,
         "activation_bytes": st["activation_bytes"],
         "hip_graph": not a.no_graph,
+        "swapin_mode": {0: "copy kernel", 1: "SDMA, calling thread", 2: "SDMA, copy thread"}[a.swapin],
     }
     if not a.no_cpu_baseline:
         log("CPU oracle baseline (~%.0f s)" % a.cpu_seconds)

@@ -238,6 +238,8 @@ typedef struct sn_piece_info {
     int64_t w_bytes, b_bytes;
     float t_ms;                 /* last inference's duration (timing level 2) */
     int32_t ksplit;             /* K splits of the layer's convolution (1: none) */
+    float t_main_ms;            /* of t_ms, the main kernel alone (a split-K
+                                   convolution's reduction kernel excluded)    */
 } sn_piece_info;
 int sn_get_piece(const sn_ctx *ctx, int j, sn_piece_info *out);
 

@@ -86,8 +86,8 @@ struct sn_ctx {
     int64_t in_bytes = 0, out_bytes = 0;
     std::vector<hipEvent_t> loaded, done;
     std::vector<hipEvent_t> t_in0, t_in1, t_ex0, t_ex1;
-    std::vector<hipEvent_t> t_p0, t_p1;   // per-piece events (timing level 2)
-    std::vector<float> piece_ms;
+    std::vector<hipEvent_t> t_p0, t_p1, t_pm;   // per-piece events (timing level 2)
+    std::vector<float> piece_ms, piece_main_ms;
     hipEvent_t t_start = nullptr;
     hipEvent_t fork = nullptr;         // start of an inference, on the compute stream
     hipEvent_t ev_end = nullptr;       // end of the previous inference
@@ -347,11 +347,14 @@ extern "C" int sn_plan(sn_ctx *c) {
     HIP_TRY(c, hipEventCreateWithFlags(&c->ev_end, hipEventDisableTiming));
     c->t_p0.assign(np, nullptr);
     c->t_p1.assign(np, nullptr);
+    c->t_pm.assign(np, nullptr);
     for (int j = 0; j < np; ++j) {
         HIP_TRY(c, hipEventCreate(&c->t_p0[j]));
         HIP_TRY(c, hipEventCreate(&c->t_p1[j]));
+        HIP_TRY(c, hipEventCreate(&c->t_pm[j]));
     }
     c->piece_ms.assign(np, 0.f);
+    c->piece_main_ms.assign(np, 0.f);
     c->slab_t_in.assign(ns, 0.f);
     c->slab_t_ex.assign(ns, 0.f);
     c->slab_t_in_start.assign(ns, 0.f);
@@ -407,7 +410,7 @@ static int run_piece(sn_ctx *c, int pi, int n_tok, hipStream_t s) {
         cp.kernel = L.kernel;
         cp.ksplit = L.ksplit;
         cp.kps = L.kps;
-        e = launch_conv(cp, a, s);
+        e = launch_conv(cp, a, s, c->timing >= 2 ? c->t_pm[pi] : nullptr);
         break;
     }
     case SN_OP_LINEAR: {
@@ -700,9 +703,15 @@ static void collect_timing(sn_ctx *c) {
     }
     if (c->timing >= 2)
         for (size_t j = 0; j < c->piece_ms.size(); ++j) {
-            float t = 0;
+            float t = 0, tm = 0;
             hipEventElapsedTime(&t, c->t_p0[j], c->t_p1[j]);
             c->piece_ms[j] = t;
+            const Layer &L = c->layers[c->plan.pieces[j].layer];
+            if (L.d.op == SN_OP_CONV2D && L.ksplit > 1)
+                hipEventElapsedTime(&tm, c->t_p0[j], c->t_pm[j]);
+            else
+                tm = t;
+            c->piece_main_ms[j] = tm;
         }
 }
 
@@ -925,6 +934,7 @@ extern "C" int sn_get_piece(const sn_ctx *c, int j, sn_piece_info *o) {
     o->w_bytes = p.w_bytes;
     o->b_bytes = p.b_bytes;
     o->t_ms = j < (int)c->piece_ms.size() ? c->piece_ms[j] : 0.f;
+    o->t_main_ms = j < (int)c->piece_main_ms.size() ? c->piece_main_ms[j] : 0.f;
     o->ksplit = c->layers[p.layer].ksplit;
     return SN_OK;
 }
@@ -951,7 +961,7 @@ extern "C" void sn_destroy(sn_ctx *c) {
         if (c->comp_s) hipStreamSynchronize(c->comp_s);
         if (c->copy_s) hipStreamSynchronize(c->copy_s);
         for (auto *v : {&c->loaded, &c->done, &c->t_in0, &c->t_in1, &c->t_ex0, &c->t_ex1, &c->t_p0,
-                        &c->t_p1})
+                        &c->t_p1, &c->t_pm})
             for (hipEvent_t e : *v)
                 if (e) hipEventDestroy(e);
         if (c->t_start) hipEventDestroy(c->t_start);

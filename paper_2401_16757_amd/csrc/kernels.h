@@ -69,7 +69,9 @@ ConvPlan conv_plan(int M, int N, int K, int cin_p, bool is1x1, bool allow_split)
 int64_t conv_workspace_bytes(const ConvPlan &p, int M, int N);
 int conv_kernel_count();
 const char *conv_kernel_name(int id);
-hipError_t launch_conv(const ConvPlan &p, ConvArgs a, hipStream_t s);
+// `mid` (optional): event recorded between the split-K main kernel and its
+// reduction kernel (profiling).
+hipError_t launch_conv(const ConvPlan &p, ConvArgs a, hipStream_t s, hipEvent_t mid = nullptr);
 hipError_t launch_gemv(const GemvArgs &a, hipStream_t s);
 
 hipError_t launch_maxpool(const void *x, void *y, int H, int W, int Cp, int Ho, int Wo, int k,

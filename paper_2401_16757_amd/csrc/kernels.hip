@@ -512,32 +512,50 @@ const char *conv_kernel_name(int id) {
 // channels.  A separate kernel: the kernel boundary orders the partial-sum
 // writes of all splits (on any XCD) before these reads.
 __global__ void splitk_reduce_kernel(ConvArgs a) {
+    // four consecutive channels per thread
+    const int nq = (a.n_cover + 3) / 4;
     long t = (long)blockIdx.x * blockDim.x + threadIdx.x;
-    if (t >= (long)a.M * a.n_cover) return;
-    const int m = (int)(t / a.n_cover), n = (int)(t - (long)m * a.n_cover);
+    if (t >= (long)a.M * nq) return;
+    const int m = (int)(t / nq), n = (int)(t - (long)m * nq) * 4;
     _Float16 *yg = (_Float16 *)a.y;
     const long idx = (long)m * a.ldy + a.n0 + n;
-    if (n >= a.N) {
-        if (a.n0 + n < a.n_zero_end) yg[idx] = (_Float16)0.0f;
-        return;
-    }
     const long plane = (long)a.M * a.N;
     const float *p = a.ws + (long)m * a.N + n;
-    // loads issued eight at a time, added strictly in split order
-    float v = 0.0f;
-    int s = 0;
-    for (; s + 8 <= a.ksplit; s += 8) {
-        float q[8];
+    float v[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    if (n + 4 <= a.N && (a.N % 4) == 0) {
+        // loads issued eight splits at a time, added strictly in split order
+        int s = 0;
+        for (; s + 8 <= a.ksplit; s += 8) {
+            f4 q[8];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) q[e] = p[(long)(s + e) * plane];
+            for (int e = 0; e < 8; ++e) q[e] = *(const f4 *)(p + (long)(s + e) * plane);
 #pragma unroll
-        for (int e = 0; e < 8; ++e) v += q[e];
+            for (int e = 0; e < 8; ++e)
+#pragma unroll
+                for (int c = 0; c < 4; ++c) v[c] += q[e][c];
+        }
+        for (; s < a.ksplit; ++s) {
+            f4 q = *(const f4 *)(p + (long)s * plane);
+#pragma unroll
+            for (int c = 0; c < 4; ++c) v[c] += q[c];
+        }
+    } else {
+        for (int c = 0; c < 4; ++c)
+            if (n + c < a.N)
+                for (int s = 0; s < a.ksplit; ++s) v[c] += p[(long)s * plane + c];
     }
-    for (; s < a.ksplit; ++s) v += p[(long)s * plane];
-    if (a.bias) v += (float)((const _Float16 *)a.bias)[n];
-    if (a.res) v += (float)((const _Float16 *)a.res)[idx];
-    if (a.relu) v = fmaxf(v, 0.0f);
-    yg[idx] = (_Float16)v;
+    for (int c = 0; c < 4; ++c) {
+        const int nc = n + c;
+        if (nc >= a.N) {
+            if (nc < a.n_cover && a.n0 + nc < a.n_zero_end) yg[idx + c] = (_Float16)0.0f;
+            continue;
+        }
+        float x = v[c];
+        if (a.bias) x += (float)((const _Float16 *)a.bias)[nc];
+        if (a.res) x += (float)((const _Float16 *)a.res)[idx + c];
+        if (a.relu) x = fmaxf(x, 0.0f);
+        yg[idx + c] = (_Float16)x;
+    }
 }
 
 static int find_variant(int bm, int bn, int kind) {
@@ -571,7 +589,10 @@ ConvPlan conv_plan(int M, int N, int K, int cin_p, bool is1x1, bool allow_split)
     long blocks = (long)((M + 63) / 64) * ((N + 63) / 64);
     const int kt = (K + v.bk - 1) / v.bk;
     const int min_tiles = v.bk == 64 ? 2 : 4;
-    int s = allow_split ? (int)std::min<long>((target + blocks - 1) / blocks, kt / min_tiles) : 1;
+    // the reduction kernel costs about as much as a dozen K tiles of a
+    // latency-bound block: short K ranges are not split
+    const bool long_k = K >= 768;
+    int s = allow_split && long_k ? (int)std::min<long>((target + blocks - 1) / blocks, kt / min_tiles) : 1;
     if (s < 2) {
         p.kps = K;
         return p;
@@ -591,7 +612,7 @@ int64_t conv_workspace_bytes(const ConvPlan &p, int M, int N) {
 }
 
 
-hipError_t launch_conv(const ConvPlan &p, ConvArgs a, hipStream_t s) {
+hipError_t launch_conv(const ConvPlan &p, ConvArgs a, hipStream_t s, hipEvent_t mid) {
     if (p.kernel < 0 || p.kernel >= kNumConvVariants) return hipErrorInvalidValue;
     const ConvVariant &v = kConvVariants[p.kernel];
     if (a.M <= 0 || a.N <= 0) return hipSuccess;
@@ -603,7 +624,8 @@ hipError_t launch_conv(const ConvPlan &p, ConvArgs a, hipStream_t s) {
     hipLaunchKernelGGL(v.fn, dim3((unsigned)blocks, (unsigned)a.ksplit), dim3(v.threads), 0, s, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || a.ksplit == 1) return e;
-    long n = (long)a.M * a.n_cover;
+    if (mid && (e = hipEventRecord(mid, s)) != hipSuccess) return e;
+    long n = (long)a.M * ((a.n_cover + 3) / 4);
     hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, a);
     return hipGetLastError();
 }

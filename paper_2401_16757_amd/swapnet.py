@@ -66,7 +66,7 @@ class SnPieceInfo(C.Structure):
     _fields_ = [("layer", C.c_int32), ("c0", C.c_int32), ("c1", C.c_int32),
                 ("kernel", C.c_int32), ("w_off", C.c_int64), ("b_off", C.c_int64),
                 ("w_bytes", C.c_int64), ("b_bytes", C.c_int64), ("t_ms", C.c_float),
-                ("ksplit", C.c_int32)]
+                ("ksplit", C.c_int32), ("t_main_ms", C.c_float)]
 
 
 _lib = None

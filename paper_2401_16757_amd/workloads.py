@@ -13,8 +13,9 @@ weights or datasets are used: every tensor is synthetic.
 Seeding (one stream per tensor, so any tensor can be regenerated alone):
   weights of layer ``li``, tensor ``ti``  -> SeedSequence([cfg, 0, li, ti])
   network input                            -> SeedSequence([cfg, 1])
-Draws are fp64; folding of batch-norm statistics is done in fp64; every
-stored tensor is then rounded once to fp16 (round-to-nearest-even).
+Draws are fp64 (the decoder's N(0, 0.02) tensors: fp32, to keep the 6.7B
+generator near a minute); folding of batch-norm statistics is done in fp64;
+every stored tensor is then rounded once to fp16 (round-to-nearest-even).
 
 Batch-norm statistics are data-independent (running mean ~ N(0, 0.1),
 running variance ~ U(0.5, 1.5), gamma ~ U(0.5, 1.5), beta ~ N(0, 0.1)); the
@@ -24,7 +25,9 @@ O(1) at depth 33 instead of overflowing fp16.
 """
 from __future__ import annotations
 
+import concurrent.futures
 import math
+import os
 from dataclasses import dataclass, field
 
 import numpy as np
@@ -385,9 +388,15 @@ def layer_params(net, li):
         out["weight"] = w.astype(np.float16)
         out["bias"] = b.astype(np.float16)
     elif layer.op == "linear":
-        std = layer.w_std or math.sqrt(2.0 / layer.c_in)
-        out["weight"] = rng_for(cfg, 0, li, 0).normal(0.0, std, (layer.c_out, layer.c_in)
-                                                      ).astype(np.float16)
+        if layer.w_std:
+            # decoder projections: float32 draws (see the other decoder tensors)
+            a = rng_for(cfg, 0, li, 0).standard_normal((layer.c_out, layer.c_in), dtype=np.float32)
+            a *= np.float32(layer.w_std)
+            out["weight"] = a.astype(np.float16)
+        else:
+            std = math.sqrt(2.0 / layer.c_in)
+            out["weight"] = rng_for(cfg, 0, li, 0).normal(0.0, std, (layer.c_out, layer.c_in)
+                                                          ).astype(np.float16)
         if layer.bias_std > 0:
             out["bias"] = rng_for(cfg, 0, li, 5).normal(0.0, layer.bias_std, layer.c_out
                                                         ).astype(np.float16)
@@ -403,9 +412,21 @@ def layer_params(net, li):
     return out
 
 
-def make_weights(net):
+def layers_params(net, indices, threads=None):
+    """{li: params} for the given layers, generated on a thread pool (every
+    tensor has its own seed, so the result does not depend on the order)."""
+    indices = list(indices)
+    threads = threads or min(16, os.cpu_count() or 1)
+    if threads <= 1 or len(indices) <= 1:
+        return {li: layer_params(net, li) for li in indices}
+    with concurrent.futures.ThreadPoolExecutor(threads) as ex:
+        return dict(zip(indices, ex.map(lambda li: layer_params(net, li), indices)))
+
+
+def make_weights(net, threads=None):
     """List (per layer) of dicts of fp16 canonical parameter arrays."""
-    return [layer_params(net, li) for li in range(len(net.layers))]
+    p = layers_params(net, range(len(net.layers)), threads)
+    return [p[li] for li in range(len(net.layers))]
 
 
 def make_input(net, seed_word=1):

@@ -201,3 +201,32 @@ def test_decoder_prefill_uses_mfma_path_and_decode_matches_prefix():
     ref = oracle.decoder_forward(net, wts, prompt)[-1]
     assert rel_err(a, ref) <= TOL
     assert rel_err(b, ref) <= TOL
+
+
+@pytest.mark.slow
+def test_decoder_full_width_two_layers():
+    """Full 7B layer shapes (d 4096, 32 heads, SwiGLU 11008, vocab 32000), two
+    layers, a 512-token prompt (prefill on the MFMA GEMM path) and four decode
+    steps (GEMV path), swapped at a budget of one layer's weights plus change,
+    teacher-forced against the oracle."""
+    net = W.decoder7b(n_layers=2, max_seq=520, prompt=512, gen=4)
+    print("[case] decoder full width, generating weights", flush=True)
+    wts = W.make_weights(net)
+    prompt = W.make_input(net)
+    layer_bytes = sum(l.weight_bytes() for l in net.layers[1:8])
+    eng = S.build_engine(net, wts, budget=int(layer_bytes * 1.2))
+    st = eng.stats()
+    assert st["resident"] == 0 and st["n_slabs"] >= 3
+    rows, fed = [eng.infer_tokens(prompt)], []
+    for _ in range(3):
+        nxt = int(np.argmax(rows[-1]))
+        fed.append(nxt)
+        rows.append(eng.infer_tokens(np.array([nxt], np.int32)))
+    eng.close()
+    print("[case] decoder full width, oracle", flush=True)
+    seq = np.concatenate([prompt, np.array(fed, np.int32)])
+    ref = oracle.decoder_forward(net, wts, seq)[len(prompt) - 1:]
+    for t in range(4):
+        e = rel_err(rows[t], ref[t])
+        print(f"  step {t}: rel err {e:.2e}", flush=True)
+        assert e <= TOL
