@@ -170,6 +170,12 @@ enum sn_option {
                                    (uses compute units, never blocks)         */
     SN_OPT_SWAPIN_BLOCKS = 6,   /* workgroups of the swap-in copy kernel
                                    (default 32)                               */
+    SN_OPT_COPY_STREAMS = 7,    /* DMA queues used by the copy thread: 1
+                                   (default) a single queue; 2 alternates
+                                   consecutive slabs between two queues so
+                                   that one queue's per-copy start-up overlaps
+                                   the other's transfer (the two then share
+                                   the link, which delays each slab)          */
     SN_OPT_GRAPH = 4            /* 1 (default): the kernels of each slab of an
                                    image network are captured once per
                                    (input, output) buffer pair into one HIP

@@ -53,6 +53,8 @@ struct sn_ctx {
     int device = 0;
     uint8_t *arena = nullptr;
     hipStream_t copy_s = nullptr, comp_s = nullptr;
+    hipStream_t copy_s2 = nullptr;     // second DMA queue (copy thread, SN_OPT_COPY_STREAMS = 2)
+    int copy_streams = 1;
     uint8_t *image = nullptr;          // pinned (device mode) or malloc (host-only)
     uint8_t *image_dev = nullptr;      // the pinned image as seen from the device
     int swapin = 2;                    // see SN_OPT_SWAPIN
@@ -139,6 +141,7 @@ extern "C" sn_ctx *sn_create_ex(size_t budget_bytes, int flags) {
         hipError_t e = hipGetDevice(&c->device);
         if (e == hipSuccess) e = hipMalloc((void **)&c->arena, (size_t)c->budget);
         if (e == hipSuccess) e = hipStreamCreateWithFlags(&c->copy_s, hipStreamNonBlocking);
+        if (e == hipSuccess) e = hipStreamCreateWithFlags(&c->copy_s2, hipStreamNonBlocking);
         if (e == hipSuccess) e = hipStreamCreateWithFlags(&c->comp_s, hipStreamNonBlocking);
         if (e != hipSuccess) {
             g_create_err = std::string("device setup failed: ") + hipGetErrorString(e);
@@ -209,6 +212,11 @@ extern "C" int sn_set_option(sn_ctx *c, int option, int64_t value) {
         return SN_OK;
     case SN_OPT_GRAPH:
         c->use_graph = value != 0;
+        return SN_OK;
+    case SN_OPT_COPY_STREAMS:
+        if (value != 1 && value != 2) return fail(c, SN_E_INVALID, "copy streams must be 1 or 2");
+        if (c->state == ST_PLANNED && c->have_prev) wait_copier_idle(c);
+        c->copy_streams = (int)value;
         return SN_OK;
     case SN_OPT_MAX_SLAB:
         if (c->state != ST_ADDING) return fail(c, SN_E_STATE, "max slab is fixed at plan");
@@ -515,15 +523,29 @@ static void copier_main(sn_ctx *c) {
     const int ns = (int)c->plan.slabs.size();
     for (;;) {
         uint64_t seq;
+        // spin briefly for the next inference (back-to-back calls), then sleep
+        auto spin_until = std::chrono::steady_clock::now() + std::chrono::milliseconds(2);
+        bool have = false;
+        while (std::chrono::steady_clock::now() < spin_until) {
+            if (c->fork_seq.load(std::memory_order_acquire) > c->handled.load()) {
+                have = true;
+                break;
+            }
+            for (int k = 0; k < 32; ++k) cpu_relax();
+        }
         {
             std::unique_lock<std::mutex> lk(c->mu);
-            c->cv.wait(lk, [&] { return c->stop || c->requested > c->handled.load(); });
+            if (!have)
+                c->cv.wait(lk, [&] { return c->stop || c->requested > c->handled.load(); });
             if (c->stop) return;
             seq = c->handled.load() + 1;
         }
         bool aborted = false;
         for (int i = 0; i < ns && !aborted; ++i) {
             const Slab &s = c->plan.slabs[i];
+            // consecutive slabs alternate between two DMA queues, so that one
+            // queue's per-copy start-up overlaps the other's transfer
+            hipStream_t q = (c->copy_streams == 2 && (i & 1)) ? c->copy_s2 : c->copy_s;
             std::atomic<uint64_t> &gate = s.wait >= 0 ? c->done_seq[s.wait] : c->fork_seq;
             hipEvent_t ev = s.wait >= 0 ? c->done[s.wait] : c->fork;
             while (gate.load(std::memory_order_acquire) < seq) {
@@ -538,12 +560,12 @@ static void copier_main(sn_ctx *c) {
             while ((e = hipEventQuery(ev)) == hipErrorNotReady) {
                 for (int k = 0; k < 64; ++k) cpu_relax();
             }
-            if (e == hipSuccess && c->timing) e = hipEventRecord(c->t_in0[i], c->copy_s);
+            if (e == hipSuccess && c->timing) e = hipEventRecord(c->t_in0[i], q);
             if (e == hipSuccess && s.bytes)
                 e = hipMemcpyAsync(c->arena + s.arena_off, c->image + s.image_off, (size_t)s.bytes,
-                                   hipMemcpyHostToDevice, c->copy_s);
-            if (e == hipSuccess && c->timing) e = hipEventRecord(c->t_in1[i], c->copy_s);
-            if (e == hipSuccess) e = hipEventRecord(c->loaded[i], c->copy_s);
+                                   hipMemcpyHostToDevice, q);
+            if (e == hipSuccess && c->timing) e = hipEventRecord(c->t_in1[i], q);
+            if (e == hipSuccess) e = hipEventRecord(c->loaded[i], q);
             if (e != hipSuccess && !c->copy_error.load()) {
                 c->copy_err = std::string("swap-in DMA: ") + hipGetErrorString(e);
                 c->copy_error.store(1);
@@ -826,6 +848,7 @@ extern "C" int sn_infer(sn_ctx *c, const void *input, void *output) {
     if (rc) {
         hipStreamSynchronize(c->comp_s);
         hipStreamSynchronize(c->copy_s);
+        hipStreamSynchronize(c->copy_s2);
         return rc;
     }
     HIP_TRY(c, hipMemcpyAsync(output, c->out_stage, (size_t)c->out_bytes, hipMemcpyDeviceToHost, c->comp_s));
@@ -854,6 +877,7 @@ extern "C" int sn_infer_tokens(sn_ctx *c, const int32_t *ids, int n_ids, float *
     if (rc) {
         hipStreamSynchronize(cs);
         hipStreamSynchronize(c->copy_s);
+        hipStreamSynchronize(c->copy_s2);
         return rc;
     }
     HIP_TRY(c, hipMemcpyAsync(logits, slot_ptr(c, c->layers.back().d.dst), (size_t)c->out_bytes,
@@ -960,6 +984,7 @@ extern "C" void sn_destroy(sn_ctx *c) {
     if (!c->host_only) {
         if (c->comp_s) hipStreamSynchronize(c->comp_s);
         if (c->copy_s) hipStreamSynchronize(c->copy_s);
+        if (c->copy_s2) hipStreamSynchronize(c->copy_s2);
         for (auto *v : {&c->loaded, &c->done, &c->t_in0, &c->t_in1, &c->t_ex0, &c->t_ex1, &c->t_p0,
                         &c->t_p1, &c->t_pm})
             for (hipEvent_t e : *v)
@@ -974,6 +999,7 @@ extern "C" void sn_destroy(sn_ctx *c) {
                         (void *)c->q_scratch, c->in_stage, c->out_stage, (void *)c->ws})
             if (p) hipFree(p);
         if (c->copy_s) hipStreamDestroy(c->copy_s);
+        if (c->copy_s2) hipStreamDestroy(c->copy_s2);
         if (c->comp_s) hipStreamDestroy(c->comp_s);
     } else {
         free(c->image);

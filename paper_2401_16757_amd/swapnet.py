@@ -27,6 +27,7 @@ OP = {"conv2d": 1, "linear": 2, "maxpool": 3, "gavgpool": 4, "upsample_bilinear"
 FLAG_RELU, FLAG_FLATTEN_CHW, FLAG_SWIGLU, FLAG_OUT_F32, FLAG_LAST_ROW = 1, 2, 4, 8, 16
 CREATE_HOST_ONLY = 1
 OPT_SPLIT_BUDGET, OPT_TIMING, OPT_MAX_SLAB, OPT_GRAPH, OPT_SWAPIN, OPT_SWAPIN_BLOCKS = 1, 2, 3, 4, 5, 6
+OPT_COPY_STREAMS = 7
 
 EXPORTS = ["sn_create", "sn_create_ex", "sn_add_block", "sn_plan", "sn_set_option", "sn_infer",
            "sn_infer_dev", "sn_infer_tokens", "sn_reset", "sn_get_stats", "sn_get_slab",
