@@ -69,7 +69,10 @@ struct sn_ctx {
     uint64_t seq = 0;                  // inference sequence number (main thread)
     std::atomic<uint64_t> handled{0};  // last inference whose copies were all issued
     std::atomic<uint64_t> fork_seq{0}, abort_seq{0};
-    std::unique_ptr<std::atomic<uint64_t>[]> done_seq, loaded_seq;
+    std::unique_ptr<std::atomic<uint64_t>[]> loaded_seq;
+    // completion counters written by the compute stream (signal kernels) in
+    // pinned host memory: [0, ns) per slab, ns = inference start
+    unsigned long long *sig_host = nullptr, *sig_dev = nullptr;
     std::atomic<int> copy_error{0};
     std::string copy_err;
     uint8_t *act = nullptr;
@@ -106,12 +109,18 @@ struct sn_ctx {
 
 static thread_local std::string g_create_err;
 static void wait_copier_idle(sn_ctx *c);
+static void drop_graphs(sn_ctx *c);
 static void start_copier(sn_ctx *c);
 static void stop_copier(sn_ctx *c);
 
 static int fail(sn_ctx *c, int code, const std::string &msg) {
     if (c) c->err = msg;
     return code;
+}
+
+static hipError_t ensure_stream(hipStream_t *s) {
+    if (*s) return hipSuccess;
+    return hipStreamCreateWithFlags(s, hipStreamNonBlocking);
 }
 
 #define HIP_TRY(ctx, call)                                                                       \
@@ -140,9 +149,9 @@ extern "C" sn_ctx *sn_create_ex(size_t budget_bytes, int flags) {
     if (!c->host_only) {
         hipError_t e = hipGetDevice(&c->device);
         if (e == hipSuccess) e = hipMalloc((void **)&c->arena, (size_t)c->budget);
-        if (e == hipSuccess) e = hipStreamCreateWithFlags(&c->copy_s, hipStreamNonBlocking);
-        if (e == hipSuccess) e = hipStreamCreateWithFlags(&c->copy_s2, hipStreamNonBlocking);
-        if (e == hipSuccess) e = hipStreamCreateWithFlags(&c->comp_s, hipStreamNonBlocking);
+        // streams are created when first needed: every stream takes one of
+        // the process's few hardware queues, and queues shared between a copy
+        // stream and a compute stream serialise them
         if (e != hipSuccess) {
             g_create_err = std::string("device setup failed: ") + hipGetErrorString(e);
             sn_destroy(c);
@@ -204,6 +213,7 @@ extern "C" int sn_set_option(sn_ctx *c, int option, int64_t value) {
     case SN_OPT_SWAPIN:
         if (value < 0 || value > 2) return fail(c, SN_E_INVALID, "swap-in mode must be 0, 1 or 2");
         if (c->state == ST_PLANNED && c->have_prev) wait_copier_idle(c);
+        if (c->swapin != (int)value) drop_graphs(c);
         c->swapin = (int)value;
         return SN_OK;
     case SN_OPT_SWAPIN_BLOCKS:
@@ -216,6 +226,8 @@ extern "C" int sn_set_option(sn_ctx *c, int option, int64_t value) {
     case SN_OPT_COPY_STREAMS:
         if (value != 1 && value != 2) return fail(c, SN_E_INVALID, "copy streams must be 1 or 2");
         if (c->state == ST_PLANNED && c->have_prev) wait_copier_idle(c);
+        if (value == 2 && c->state == ST_PLANNED && !c->host_only && !c->plan.resident)
+            HIP_TRY(c, ensure_stream(&c->copy_s2));
         c->copy_streams = (int)value;
         return SN_OK;
     case SN_OPT_MAX_SLAB:
@@ -368,14 +380,21 @@ extern "C" int sn_plan(sn_ctx *c) {
     c->slab_t_in_start.assign(ns, 0.f);
     c->slab_t_ex_start.assign(ns, 0.f);
 
-    if (!c->plan.resident) start_copier(c);
+    if (!c->plan.resident) {
+        HIP_TRY(c, ensure_stream(&c->copy_s));
+        if (c->copy_streams == 2) HIP_TRY(c, ensure_stream(&c->copy_s2));
+        HIP_TRY(c, hipHostMalloc((void **)&c->sig_host, (ns + 1) * sizeof(unsigned long long),
+                                 hipHostMallocMapped));
+        memset(c->sig_host, 0, (ns + 1) * sizeof(unsigned long long));
+        HIP_TRY(c, hipHostGetDevicePointer((void **)&c->sig_dev, c->sig_host, 0));
+        start_copier(c);
+    }
     if (c->plan.resident) {
         // everything fits: one upload now, no swapping per inference
         for (const Slab &s : c->plan.slabs)
             if (s.bytes)
-                HIP_TRY(c, hipMemcpyAsync(c->arena + s.arena_off, c->image + s.image_off,
-                                          (size_t)s.bytes, hipMemcpyHostToDevice, c->copy_s));
-        HIP_TRY(c, hipStreamSynchronize(c->copy_s));
+                HIP_TRY(c, hipMemcpy(c->arena + s.arena_off, c->image + s.image_off,
+                                     (size_t)s.bytes, hipMemcpyHostToDevice));
     }
     c->state = ST_PLANNED;
     return SN_OK;
@@ -546,9 +565,10 @@ static void copier_main(sn_ctx *c) {
             // consecutive slabs alternate between two DMA queues, so that one
             // queue's per-copy start-up overlaps the other's transfer
             hipStream_t q = (c->copy_streams == 2 && (i & 1)) ? c->copy_s2 : c->copy_s;
-            std::atomic<uint64_t> &gate = s.wait >= 0 ? c->done_seq[s.wait] : c->fork_seq;
-            hipEvent_t ev = s.wait >= 0 ? c->done[s.wait] : c->fork;
-            while (gate.load(std::memory_order_acquire) < seq) {
+            // the compute this slab's DMA must follow has completed once its
+            // counter reaches `seq` (no runtime call while waiting)
+            volatile unsigned long long *gate = c->sig_host + (s.wait >= 0 ? s.wait : ns);
+            while (*gate < seq) {
                 if (c->abort_seq.load() >= seq) {
                     aborted = true;
                     break;
@@ -556,10 +576,7 @@ static void copier_main(sn_ctx *c) {
                 cpu_relax();
             }
             if (aborted) break;
-            hipError_t e;
-            while ((e = hipEventQuery(ev)) == hipErrorNotReady) {
-                for (int k = 0; k < 64; ++k) cpu_relax();
-            }
+            hipError_t e = hipSuccess;
             if (e == hipSuccess && c->timing) e = hipEventRecord(c->t_in0[i], q);
             if (e == hipSuccess && s.bytes)
                 e = hipMemcpyAsync(c->arena + s.arena_off, c->image + s.image_off, (size_t)s.bytes,
@@ -585,12 +602,8 @@ static void wait_copier_idle(sn_ctx *c) {
 
 static void start_copier(sn_ctx *c) {
     const int ns = (int)c->plan.slabs.size();
-    c->done_seq.reset(new std::atomic<uint64_t>[ns]);
     c->loaded_seq.reset(new std::atomic<uint64_t>[ns]);
-    for (int i = 0; i < ns; ++i) {
-        c->done_seq[i].store(0);
-        c->loaded_seq[i].store(0);
-    }
+    for (int i = 0; i < ns; ++i) c->loaded_seq[i].store(0);
     c->copier = std::thread(copier_main, c);
 }
 
@@ -672,6 +685,8 @@ static int run_slabs(sn_ctx *c, int n_tok, hipStream_t cs, Pre pre, Post post, b
         return SN_OK;
     };
     if (threaded) {
+        hipError_t e = launch_signal(c->sig_dev + ns, cs);
+        if (e != hipSuccess) return abort_copies(fail(c, SN_E_HIP, std::string("signal: ") + hipGetErrorString(e)));
         c->fork_seq.store(seq, std::memory_order_release);
         {
             std::lock_guard<std::mutex> lk(c->mu);
@@ -697,12 +712,13 @@ static int run_slabs(sn_ctx *c, int n_tok, hipStream_t cs, Pre pre, Post post, b
             if (i == 0 && (rc = pre(cs))) return abort_copies(rc);
             if ((rc = slab_kernels(c, i, n_tok, cs))) return abort_copies(rc);
             if (i == ns - 1 && (rc = post(cs))) return abort_copies(rc);
+            if (threaded && (e = launch_signal(c->sig_dev + i, cs)) != hipSuccess)
+                return abort_copies(fail(c, SN_E_HIP, std::string("signal: ") + hipGetErrorString(e)));
         }
         if (c->timing) e = hipEventRecord(c->t_ex1[i], cs);
         if (e == hipSuccess) e = hipEventRecord(c->done[i], cs);
         if (e != hipSuccess) return abort_copies(fail(c, SN_E_HIP, hipGetErrorString(e)));
-        if (threaded) c->done_seq[i].store(seq, std::memory_order_release);
-        else if ((rc = issue(i))) return rc;
+        if (!threaded && (rc = issue(i))) return rc;
     }
     return SN_OK;
 }
@@ -785,6 +801,7 @@ static void drop_graphs(sn_ctx *c) {
 // the ordering events stay outside the graphs.
 static int capture_graphs(sn_ctx *c, const void *d_in, void *d_out) {
     drop_graphs(c);
+    HIP_TRY(c, ensure_stream(&c->comp_s));
     const int ns = (int)c->plan.slabs.size();
     c->graphs.assign(ns, nullptr);
     for (int i = 0; i < ns; ++i) {
@@ -793,6 +810,10 @@ static int capture_graphs(sn_ctx *c, const void *d_in, void *d_out) {
         if (i == 0) rc = convert_input(c, d_in, c->comp_s);
         if (!rc) rc = slab_kernels(c, i, 1, c->comp_s);
         if (!rc && i == ns - 1) rc = convert_output(c, d_out, c->comp_s);
+        if (!rc && !c->plan.resident && c->swapin == 2) {
+            hipError_t e = launch_signal(c->sig_dev + i, c->comp_s);
+            if (e != hipSuccess) rc = fail(c, SN_E_HIP, std::string("signal: ") + hipGetErrorString(e));
+        }
         hipGraph_t g = nullptr;
         hipError_t e = hipStreamEndCapture(c->comp_s, &g);
         if (!rc && e != hipSuccess)
@@ -834,6 +855,7 @@ extern "C" int sn_infer_dev(sn_ctx *c, const void *d_in, void *d_out, void *hip_
     int rc = check_ready(c, false);
     if (rc) return rc;
     if (!d_in || !d_out) return fail(c, SN_E_INVALID, "NULL buffer");
+    if (!hip_stream) HIP_TRY(c, ensure_stream(&c->comp_s));
     hipStream_t cs = hip_stream ? (hipStream_t)hip_stream : c->comp_s;
     return infer_dev_impl(c, d_in, d_out, cs);
 }
@@ -843,12 +865,13 @@ extern "C" int sn_infer(sn_ctx *c, const void *input, void *output) {
     if (rc) return rc;
     if (!input || !output) return fail(c, SN_E_INVALID, "NULL buffer");
     auto t0 = std::chrono::steady_clock::now();
+    HIP_TRY(c, ensure_stream(&c->comp_s));
     HIP_TRY(c, hipMemcpyAsync(c->in_stage, input, (size_t)c->in_bytes, hipMemcpyHostToDevice, c->comp_s));
     rc = infer_dev_impl(c, c->in_stage, c->out_stage, c->comp_s);
     if (rc) {
         hipStreamSynchronize(c->comp_s);
-        hipStreamSynchronize(c->copy_s);
-        hipStreamSynchronize(c->copy_s2);
+        if (c->copy_s) hipStreamSynchronize(c->copy_s);
+        if (c->copy_s2) hipStreamSynchronize(c->copy_s2);
         return rc;
     }
     HIP_TRY(c, hipMemcpyAsync(output, c->out_stage, (size_t)c->out_bytes, hipMemcpyDeviceToHost, c->comp_s));
@@ -869,6 +892,7 @@ extern "C" int sn_infer_tokens(sn_ctx *c, const int32_t *ids, int n_ids, float *
     for (int i = 0; i < n_ids; ++i)
         if (ids[i] < 0 || ids[i] >= vocab) return fail(c, SN_E_INVALID, "token id out of range");
     auto t0 = std::chrono::steady_clock::now();
+    HIP_TRY(c, ensure_stream(&c->comp_s));
     hipStream_t cs = c->comp_s;
     if (c->have_prev) HIP_TRY(c, hipStreamWaitEvent(cs, c->ev_end, 0));
     HIP_TRY(c, hipMemcpyAsync(c->d_ids, ids, (size_t)n_ids * 4, hipMemcpyHostToDevice, cs));
@@ -876,8 +900,8 @@ extern "C" int sn_infer_tokens(sn_ctx *c, const int32_t *ids, int n_ids, float *
     rc = run_slabs(c, n_ids, cs, none, none, false);
     if (rc) {
         hipStreamSynchronize(cs);
-        hipStreamSynchronize(c->copy_s);
-        hipStreamSynchronize(c->copy_s2);
+        if (c->copy_s) hipStreamSynchronize(c->copy_s);
+        if (c->copy_s2) hipStreamSynchronize(c->copy_s2);
         return rc;
     }
     HIP_TRY(c, hipMemcpyAsync(logits, slot_ptr(c, c->layers.back().d.dst), (size_t)c->out_bytes,
@@ -995,6 +1019,7 @@ extern "C" void sn_destroy(sn_ctx *c) {
         drop_graphs(c);
         if (c->image) hipHostFree(c->image);
         if (c->table_host) hipHostFree(c->table_host);
+        if (c->sig_host) hipHostFree(c->sig_host);
         for (void *p : {(void *)c->arena, (void *)c->act, (void *)c->kv, (void *)c->d_ids,
                         (void *)c->q_scratch, c->in_stage, c->out_stage, (void *)c->ws})
             if (p) hipFree(p);

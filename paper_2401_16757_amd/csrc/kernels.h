@@ -88,6 +88,11 @@ hipError_t launch_hwc_to_chw(const void *x, void *y, int C, int H, int W, int Cp
 hipError_t launch_swapin(const void *src_host_mapped, void *dst, int64_t bytes, int blocks,
                          hipStream_t s);
 
+// Completion signal: increments *flag (a counter in pinned host memory,
+// device-mapped) once all earlier work on the stream has finished.  The host
+// polls the counter without any runtime call.
+hipError_t launch_signal(unsigned long long *flag, hipStream_t s);
+
 hipError_t launch_embed(const int32_t *ids, const void *table, void *y, int T, int d, hipStream_t s);
 hipError_t launch_rmsnorm(const void *x, const void *gain, void *y, int T, int d, float eps,
                           hipStream_t s);

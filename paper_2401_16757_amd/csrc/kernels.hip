@@ -388,8 +388,8 @@ __global__ __launch_bounds__(WM *WN * 64) void conv_mfma2_kernel(ConvArgs a) {
         tap_s = rs - tap_r * a.kw;
     }
 
-    h8 ra[A_CH], rb[B_CH];
-    auto load_tile = [&](int k0) {
+    h8 ra0[A_CH], rb0[B_CH], ra1[A_CH], rb1[B_CH];
+    auto load_tile = [&](int k0, h8 (&ra)[A_CH], h8 (&rb)[B_CH]) {
         const int k = k0 + kc * 8;
         const bool kok = k < kend;
 #pragma unroll
@@ -420,7 +420,7 @@ __global__ __launch_bounds__(WM *WN * 64) void conv_mfma2_kernel(ConvArgs a) {
             }
         }
     };
-    auto store_tile = [&](int buf) {
+    auto store_tile = [&](int buf, const h8 (&ra)[A_CH], const h8 (&rb)[B_CH]) {
 #pragma unroll
         for (int i = 0; i < A_CH; ++i)
             *(h8 *)(&As[buf][(row_base + i * ROW_STEP) * LDK + kc * 8]) = ra[i];
@@ -440,22 +440,18 @@ __global__ __launch_bounds__(WM *WN * 64) void conv_mfma2_kernel(ConvArgs a) {
     const int lrow = lane & 31;
     const int lk = (lane >> 5) * 8;
 
-    load_tile(kbeg);
-    store_tile(0);
-    __syncthreads();
-    int cur = 0;
-    for (int k0 = kbeg; k0 < kend; k0 += BK) {
-        const bool more = k0 + BK < kend;
-        if (more) load_tile(k0 + BK);
+    // Pipeline: tile t is multiplied from LDS while tile t+1 waits in
+    // registers and the global loads of tile t+2 are in flight.
+    auto mma = [&](int buf) {
 #pragma unroll
         for (int kk = 0; kk < BK; kk += 16) {
             h8 fa[TM], fb[TN];
 #pragma unroll
             for (int i = 0; i < TM; ++i)
-                fa[i] = *(const h8 *)(&As[cur][(wm * WTM + i * 32 + lrow) * LDK + kk + lk]);
+                fa[i] = *(const h8 *)(&As[buf][(wm * WTM + i * 32 + lrow) * LDK + kk + lk]);
 #pragma unroll
             for (int j = 0; j < TN; ++j)
-                fb[j] = *(const h8 *)(&Bs[cur][(wn * WTN + j * 32 + lrow) * LDK + kk + lk]);
+                fb[j] = *(const h8 *)(&Bs[buf][(wn * WTN + j * 32 + lrow) * LDK + kk + lk]);
 #pragma unroll
             for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -463,9 +459,25 @@ __global__ __launch_bounds__(WM *WN * 64) void conv_mfma2_kernel(ConvArgs a) {
                     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fa[i], fb[j], acc[i][j],
                                                                         0, 0, 0);
         }
-        if (more) store_tile(cur ^ 1);
+    };
+    const int ntiles = (kend - kbeg + BK - 1) / BK;
+    load_tile(kbeg, ra0, rb0);
+    store_tile(0, ra0, rb0);
+    if (ntiles > 1) load_tile(kbeg + BK, ra1, rb1);
+    __syncthreads();
+    // two tiles per trip so that the register sets are named statically
+    for (int t = 0; t < ntiles; t += 2) {
+        // tile t in LDS buffer 0, tile t+1 in ra1/rb1
+        if (t + 2 < ntiles) load_tile(kbeg + (t + 2) * BK, ra0, rb0);
+        mma(0);
+        if (t + 1 < ntiles) store_tile(1, ra1, rb1);
         __syncthreads();
-        cur ^= 1;
+        if (t + 1 >= ntiles) break;
+        // tile t+1 in LDS buffer 1, tile t+2 in ra0/rb0
+        if (t + 3 < ntiles) load_tile(kbeg + (t + 3) * BK, ra1, rb1);
+        mma(1);
+        if (t + 2 < ntiles) store_tile(0, ra0, rb0);
+        __syncthreads();
     }
     static_assert(BM * (BN + 4) * 4 <= 2 * (BM + BN) * LDK * 2, "staging tile exceeds LDS");
     if (a.swiglu)
@@ -897,6 +909,15 @@ hipError_t launch_swapin(const void *src_host_mapped, void *dst, int64_t bytes, 
     unsigned grid = (unsigned)std::max<long>(1, std::min<long>(blocks, need));
     hipLaunchKernelGGL(swapin_kernel, dim3(grid), dim3(256), 0, s, (const u32x4 *)src_host_mapped,
                        (u32x4 *)dst, n16);
+    return hipGetLastError();
+}
+
+__global__ void signal_kernel(unsigned long long *flag) {
+    if (threadIdx.x == 0) *(volatile unsigned long long *)flag = *(volatile unsigned long long *)flag + 1;
+}
+
+hipError_t launch_signal(unsigned long long *flag, hipStream_t s) {
+    hipLaunchKernelGGL(signal_kernel, dim3(1), dim3(64), 0, s, flag);
     return hipGetLastError();
 }
 
