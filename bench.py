@@ -129,6 +129,21 @@ def single_latency(torch, eng, xd, yd, n=10):
     return float(np.median(ts))
 
 
+def recorded_traffic(kernel):
+    """HBM bytes per dispatch of `kernel` from the committed counter summary
+    (profiles/*_traffic.json), or None when there is none or the kernel
+    source changed since the counters were taken."""
+    import glob
+    import hashlib
+    src = os.path.join(ROOT, "paper_2401_16757_amd", "csrc", "kernels.hip")
+    digest = hashlib.sha256(open(src, "rb").read()).hexdigest()
+    for f in glob.glob(os.path.join(ROOT, "profiles", "*_traffic.json")):
+        d = json.load(open(f))
+        if d.get("kernel") == kernel and d.get("kernels_hip_sha256") == digest:
+            return d["traffic_bytes_per_dispatch"]
+    return None
+
+
 def conv_flops(spec, c0, c1):
     ho, wo = spec.out_hw()
     return 2.0 * ho * wo * (c1 - c0) * spec.c_in * spec.k * spec.k
@@ -375,7 +390,8 @@ def main():
         roofline = {"bound": "mfma", "kernel": name, "launches_per_step": launches,
                     "avg_launch_us": round(tms / launches * 1e3, 3),
                     "achieved": round(ach, 2), "peak": MFMA_FP16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                    "frac": round(ach / MFMA_FP16_PEAK_TFLOPS, 5), "traffic": None}
+                    "frac": round(ach / MFMA_FP16_PEAK_TFLOPS, 5),
+                    "traffic": recorded_traffic(name) if a.workload == "resnet50" else None}
     mfma_util = (total_flops / (res_compute_ms * 1e-3) / 1e12) / MFMA_FP16_PEAK_TFLOPS \
         if res_compute_ms > 0 else None
 
