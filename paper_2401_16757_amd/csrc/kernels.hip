@@ -14,12 +14,32 @@
 #include <math.h>
 
 #include <algorithm>
+#include <type_traits>
+#include <utility>
 
 namespace sn {
 
 typedef _Float16 h8 __attribute__((ext_vector_type(8)));
 typedef float f16v __attribute__((ext_vector_type(16)));
 typedef float f4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+// Raw buffer loads: a 16-byte load whose byte offset lies past the buffer's
+// size returns zeros, so zero padding and ragged edges need no branch.  With
+// branch-free loads the compiler counts outstanding loads exactly and the
+// prefetched K tiles stay in flight across the loop (a conditional load
+// makes it wait for every outstanding load instead).
+constexpr unsigned kOobOffset = 0x80000000u;   // buffers are smaller than 2 GiB
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *p, long bytes) {
+    // gfx9 descriptor word 3: 32-bit data format, no swizzle, byte-addressed
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), (short)0, (int)bytes,
+                                             0x00020000);
+}
+
+__device__ __forceinline__ h8 load_h8(__amdgpu_buffer_rsrc_t r, unsigned off) {
+    return __builtin_bit_cast(h8, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+}
 
 __device__ __forceinline__ h8 zero_h8() {
     h8 z;
@@ -110,87 +130,6 @@ __device__ __forceinline__ void conv_epilogue(const ConvArgs &a, f16v (&acc)[BM 
     (void)units;
 }
 
-
-// Epilogue through LDS for the double-buffered kernel: the fp32 tile is
-// staged in LDS (reusing the operand buffers), then every thread finishes
-// eight consecutive channels of one output pixel with 16-byte bias, residual
-// and output accesses (scalar accesses at ragged edges or when the piece's
-// first channel is not a multiple of 8).  K-split partial sums are written
-// the same way, in fp32.
-template <int BM, int BN, int WM, int WN, int NT>
-__device__ __forceinline__ void conv_epilogue_lds(const ConvArgs &a,
-                                                  f16v (&acc)[BM / WM / 32][BN / WN / 32],
-                                                  float *stage, int m0, int nb0, int lane, int wm,
-                                                  int wn) {
-    constexpr int WTM = BM / WM, WTN = BN / WN;
-    constexpr int TM = WTM / 32, TN = WTN / 32;
-    constexpr int LDS_N = BN + 4;
-    const int lrow = lane & 31;
-    __syncthreads();   // all waves are done reading the operand tiles
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-#pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const int ml = wm * WTM + i * 32 + (v >> 2) * 8 + (lane >> 5) * 4 + (v & 3);
-                stage[ml * LDS_N + wn * WTN + j * 32 + lrow] = acc[i][j][v];
-            }
-    __syncthreads();
-    const bool vec_ok = (a.n0 % 8) == 0;
-    _Float16 *yg = (_Float16 *)a.y;
-    const _Float16 *bg = (const _Float16 *)a.bias;
-    const _Float16 *rg = (const _Float16 *)a.res;
-    for (int c = threadIdx.x; c < BM * BN / 8; c += NT) {
-        const int ml = c / (BN / 8), nl = (c % (BN / 8)) * 8;
-        const int m = m0 + ml, n = nb0 + nl;
-        if (m >= a.M) continue;
-        float v[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) v[e] = stage[ml * LDS_N + nl + e];
-        if (a.ksplit > 1) {
-            float *ws = a.ws + (long)blockIdx.y * a.M * a.N + (long)m * a.N;
-            if (n + 8 <= a.N && (a.N % 4) == 0) {
-                *(f4 *)(ws + n) = f4{v[0], v[1], v[2], v[3]};
-                *(f4 *)(ws + n + 4) = f4{v[4], v[5], v[6], v[7]};
-            } else {
-                for (int e = 0; e < 8; ++e)
-                    if (n + e < a.N) ws[n + e] = v[e];
-            }
-            continue;
-        }
-        const long idx = (long)m * a.ldy + a.n0 + n;
-        if (vec_ok && n + 8 <= a.N) {
-            if (bg) {
-                h8 b = *(const h8 *)(bg + n);
-#pragma unroll
-                for (int e = 0; e < 8; ++e) v[e] += (float)b[e];
-            }
-            if (rg) {
-                h8 r = *(const h8 *)(rg + idx);
-#pragma unroll
-                for (int e = 0; e < 8; ++e) v[e] += (float)r[e];
-            }
-            h8 o;
-#pragma unroll
-            for (int e = 0; e < 8; ++e) o[e] = (_Float16)(a.relu ? fmaxf(v[e], 0.0f) : v[e]);
-            *(h8 *)(yg + idx) = o;
-        } else {
-            for (int e = 0; e < 8; ++e) {
-                const int ne = n + e;
-                if (ne < a.N) {
-                    float x = v[e];
-                    if (bg) x += (float)bg[ne];
-                    if (rg) x += (float)rg[idx + e];
-                    if (a.relu) x = fmaxf(x, 0.0f);
-                    yg[idx + e] = (_Float16)x;
-                } else if (a.n0 + ne < a.n_zero_end) {
-                    yg[idx + e] = (_Float16)0.0f;
-                }
-            }
-        }
-    }
-}
 
 template <int BM, int BN, int BK, int WM, int WN, bool IS1X1>
 __global__ __launch_bounds__(WM *WN * 64) void conv_mfma_kernel(ConvArgs a) {
@@ -315,102 +254,263 @@ __global__ __launch_bounds__(WM *WN * 64) void conv_mfma_kernel(ConvArgs a) {
 
 
 // ---------------------------------------------------------------------------
-// Implicit-GEMM convolution, second form: K tile of 64, double-buffered LDS
-// (one barrier per K tile; the global loads of tile t+1 are in flight while
-// tile t is multiplied), and no integer division in the K loop.
-//   MODE 0: 1x1 convolution (any stride, no padding) or token GEMM: the A
-//           row of output pixel m is one contiguous input row.
-//   MODE 1: any kernel size with Cin_p a multiple of 64: a K tile never
-//           crosses a filter tap, so the tap (r, s) and channel offset are
-//           advanced incrementally from tile to tile.
-// Same tile / wave / MFMA layout and epilogue as conv_mfma_kernel.
+// Multi-stage implicit GEMM with direct global -> LDS loads (gfx950
+// buffer_load ... lds, 16 bytes per lane).
+//
+// Block tile BM x BN, K tile 64, 4 waves in a 2 x 2 grid, S LDS stages: the
+// loads of K tile t + S - 1 are in flight while tile t is multiplied, with no
+// register staging and one barrier per K tile.  A load instruction of a wave
+// fills 8 consecutive LDS rows of 128 bytes, 16 bytes per lane; the lanes
+// pick their chunks so that chunk c of row r sits at position c ^ ((r/2) % 8)
+// and the MFMA operand reads (16 rows per LDS cycle) hit all 64 banks.  Zero padding and ragged edges are buffer reads past
+// the end (zeros).  Each stage is its own LDS variable, which lets the
+// compiler track the outstanding LDS loads per stage; the waits before each
+// barrier are explicit.
+//
+// The fp32 tile is finished through LDS 32 rows at a time: every thread
+// completes eight consecutive channels of one output pixel with 16-byte
+// accesses.  Blocks are renumbered so that each XCD (blocks are dealt to the
+// 8 XCDs round-robin) works on a contiguous range of tiles and the operand
+// panels they share stay in that XCD's L2.
 // ---------------------------------------------------------------------------
-template <int BM, int BN, int WM, int WN, int MODE>
-__global__ __launch_bounds__(WM *WN * 64) void conv_mfma2_kernel(ConvArgs a) {
-    constexpr int BK = 64;
-    constexpr int NT = WM * WN * 64;
-    constexpr int LDK = BK + 8;
-    constexpr int KC = BK / 8;
-    constexpr int A_CH = BM * KC / NT;
-    constexpr int B_CH = BN * KC / NT;
-    constexpr int WTM = BM / WM, WTN = BN / WN;
-    constexpr int TM = WTM / 32, TN = WTN / 32;
-    static_assert(BM * KC % NT == 0 && BN * KC % NT == 0, "tile/threads mismatch");
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+__device__ __forceinline__ void wait_lgkmcnt0() { __builtin_amdgcn_s_waitcnt(0xC07F); }
 
-    __shared__ __attribute__((aligned(16))) _Float16 lds[2 * (BM + BN) * LDK];
-    _Float16 (*As)[BM * LDK] = (_Float16 (*)[BM * LDK])lds;
-    _Float16 (*Bs)[BN * LDK] = (_Float16 (*)[BN * LDK])(lds + 2 * BM * LDK);
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+
+// f(integral_constant<int, 0>), ..., f(integral_constant<int, N - 1>)
+template <class F, int... J>
+__device__ __forceinline__ void static_for_impl(F &&f, std::integer_sequence<int, J...>) {
+    (f(std::integral_constant<int, J>{}), ...);
+}
+template <int N, class F>
+__device__ __forceinline__ void static_for(F &&f) {
+    static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
+
+// Buffer descriptor (gfx9 layout) of `bytes` bytes at p, in scalar registers.
+__device__ __forceinline__ i32x4 make_srd(const void *p, long bytes) {
+    const unsigned long long ad = (unsigned long long)p;
+    i32x4 r;
+    r[0] = __builtin_amdgcn_readfirstlane((int)(unsigned)ad);
+    r[1] = __builtin_amdgcn_readfirstlane((int)((ad >> 32) & 0xffffu));   // stride 0
+    r[2] = __builtin_amdgcn_readfirstlane((int)bytes);                     // num_records
+    r[3] = 0x00020000;                                                     // 32-bit data format
+    return r;
+}
+
+// LDS address (byte offset in the workgroup's LDS) of a __shared__ pointer.
+__device__ __forceinline__ unsigned lds_addr(const void *p) {
+    return (unsigned)(size_t)(const __attribute__((address_space(3))) void *)p;
+}
+
+// Direct load to LDS: lane l reads 16 bytes at byte offset voff of the
+// buffer (zeros past its end) and they land at LDS address lds_base + 16 * l.
+// Written as inline assembly so that the compiler neither reorders it against
+// LDS reads nor adds waits of its own; completion is counted by vmcnt and
+// the callers wait explicitly.  M0 (the LDS base) is saved and restored; one
+// wait state separates the M0 write from its use.
+__device__ __forceinline__ void dma16_to_lds(i32x4 srd, unsigned lds_base, unsigned voff) {
+    // both are wave-uniform by construction; this keeps them in scalar registers
+    lds_base = __builtin_amdgcn_readfirstlane(lds_base);
+#pragma unroll
+    for (int c = 0; c < 4; ++c) srd[c] = __builtin_amdgcn_readfirstlane(srd[c]);
+    unsigned saved;
+    asm volatile(
+        "s_mov_b32 %0, m0\n\t"
+        "s_mov_b32 m0, %1\n\t"
+        "s_nop 0\n\t"
+        "buffer_load_dwordx4 %2, %3, 0 offen lds\n\t"
+        "s_mov_b32 m0, %0"
+        : "=&s"(saved)
+        : "s"(lds_base), "v"(voff), "s"(srd)
+        : "memory");
+}
+
+// Bias, residual, ReLU or SwiGLU and the fp16 rounding of eight consecutive
+// weight rows n .. n+7 of output pixel m (or their fp32 K-split partials).
+__device__ __forceinline__ void finish8(const ConvArgs &a, int m, int n, float (&v)[8]) {
+    if (a.ksplit > 1) {
+        float *ws = a.ws + ((long)blockIdx.y * a.M + m) * a.N;
+        if (n + 8 <= a.N && (a.N % 4) == 0) {
+            *(f4 *)(ws + n) = f4{v[0], v[1], v[2], v[3]};
+            *(f4 *)(ws + n + 4) = f4{v[4], v[5], v[6], v[7]};
+        } else {
+            for (int e = 0; e < 8; ++e)
+                if (n + e < a.N) ws[n + e] = v[e];
+        }
+        return;
+    }
+    _Float16 *yg = (_Float16 *)a.y;
+    const _Float16 *bg = (const _Float16 *)a.bias;
+    const _Float16 *rg = (const _Float16 *)a.res;
+    if (a.swiglu) {
+        // rows come in (gate, up) pairs; unit n/2 + e = silu(gate) * up
+        const long idx = (long)m * a.ldy + a.n0 + (n >> 1);
+        for (int e = 0; e < 4; ++e) {
+            if (n + 2 * e + 1 >= a.N) break;
+            float o = silu_f(v[2 * e]) * v[2 * e + 1];
+            if (rg) o += (float)rg[idx + e];
+            yg[idx + e] = (_Float16)o;
+        }
+        return;
+    }
+    const long idx = (long)m * a.ldy + a.n0 + n;
+    if ((a.n0 % 8) == 0 && n + 8 <= a.N) {
+        if (bg) {
+            h8 b = *(const h8 *)(bg + n);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) v[e] += (float)b[e];
+        }
+        if (rg) {
+            h8 r = *(const h8 *)(rg + idx);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) v[e] += (float)r[e];
+        }
+        h8 o;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o[e] = (_Float16)(a.relu ? fmaxf(v[e], 0.0f) : v[e]);
+        *(h8 *)(yg + idx) = o;
+        return;
+    }
+    for (int e = 0; e < 8; ++e) {
+        const int ne = n + e;
+        if (ne < a.N) {
+            float x = v[e];
+            if (bg) x += (float)bg[ne];
+            if (rg) x += (float)rg[idx + e];
+            if (a.relu) x = fmaxf(x, 0.0f);
+            yg[idx + e] = (_Float16)x;
+        } else if (ne < a.n_cover && a.n0 + ne < a.n_zero_end) {
+            yg[idx + e] = (_Float16)0.0f;
+        }
+    }
+}
+
+template <int BM, int BN, int S, int MODE, int KG>
+__global__ __launch_bounds__(256 * KG) void conv_mfma3_kernel(ConvArgs a) {
+    constexpr int NW = 4 * KG, NT = 64 * NW;   // waves, threads
+    constexpr int WTM = BM / 2, WTN = BN / 2;   // wave tile (2 x 2 waves per K group)
+    constexpr int TM = WTM / 32, TN = WTN / 32;
+    constexpr int QA = BM / 8, QB = BN / 8;     // 8-row load groups per K tile
+    // Load groups per wave: NA A groups and NB B groups each, or (when the
+    // waves outnumber that split) one group per wave, A for the first QA waves.
+    constexpr bool kSplit = QA % NW == 0 && QB % NW == 0;
+    constexpr int NA = kSplit ? QA / NW : 1, NB = kSplit ? QB / NW : 1;
+    constexpr int NI = kSplit ? NA + NB : 1;    // load instructions per wave per K tile
+    constexpr int KPG = 4 / KG;                 // 16-wide K steps per group per K tile
+    constexpr int STAGE = (BM + BN) * 64;       // halves per stage
+    constexpr int LDC = BN + 4;                 // fp32 staging row
+    static_assert(KG == 1 || KG == 2 || KG == 4, "1, 2 or 4 K groups");
+    static_assert(kSplit || QA + QB == NW, "load groups per wave");
+    static_assert(S >= 3 && S <= 8, "3 to 8 stages");
+    static_assert((S - 1) * NI < 64, "vmcnt range");
+    static_assert(KG * 32 * LDC * 4 <= S * STAGE * 2, "staging tile exceeds LDS");
+    // S operand stages; the epilogue reuses the space for the fp32 partials
+    __shared__ __attribute__((aligned(16))) _Float16 smem[S * STAGE];
+    auto buf = [&](auto J) -> _Float16 * { return smem + (decltype(J)::value % S) * STAGE; };
+    float *stc = (float *)smem;
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = tid >> 6;
-    const int wm = wave / WN, wn = wave % WN;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int grp = KG > 1 ? wave >> 2 : 0;     // K group
+    const int wm = (wave >> 1) & 1, wn = wave & 1;
+
+    // XCD-contiguous tile numbering
+    const int nb = gridDim.x, bq = nb >> 3, br = nb & 7;
+    const int xcd = blockIdx.x & 7;
+    const int lb = xcd * bq + min(xcd, br) + (blockIdx.x >> 3);
     const int n_tiles = (a.n_cover + BN - 1) / BN;
-    const int tile_m = blockIdx.x / n_tiles;
-    const int tile_n = blockIdx.x % n_tiles;
-    const int m0 = tile_m * BM, nb0 = tile_n * BN;
-    const int kc = tid % KC;
-    const int row_base = tid / KC;
-    constexpr int ROW_STEP = NT / KC;
+    const int m0 = (lb / n_tiles) * BM, nb0 = (lb % n_tiles) * BN;
 
-    const _Float16 *xg = (const _Float16 *)a.x;
-    const _Float16 *wg = (const _Float16 *)a.w;
+    const i32x4 xr = make_srd(a.x, (long)a.H * a.W * a.Cin_p * 2);
+    const i32x4 wr = make_srd(a.w, (long)a.N * a.K * 2);
 
-    // per A row: input pixel origin (MODE 1) or row pointer (MODE 0)
-    int a_iy0[A_CH], a_ix0[A_CH];
-    bool a_ok[A_CH];
+    // Lane l takes row l / 8 of each 8-row group it loads and the chunk that
+    // puts chunk c of LDS row r at position c ^ ((r / 2) % 8), which spreads
+    // the 16 rows read in one LDS cycle over all 64 banks.
+    const int lr = lane >> 3;
+    const bool wave_a = kSplit || wave < QA;    // half mode: this wave loads A
+    const int qa0 = kSplit ? wave * NA : wave;  // first A group of this wave
+    const int qb0 = kSplit ? wave * NB : wave - QA;
+    int a_iy0[NA], a_ix0[NA], a_off[NA], a_ch[NA];
 #pragma unroll
-    for (int i = 0; i < A_CH; ++i) {
-        int m = m0 + row_base + i * ROW_STEP;
-        a_ok[i] = m < a.M;
-        int oy = a_ok[i] ? m / a.Wo : 0;
-        int ox = a_ok[i] ? m - oy * a.Wo : 0;
-        a_iy0[i] = oy * a.stride - a.pad;
-        a_ix0[i] = ox * a.stride - a.pad;
+    for (int u = 0; u < NA; ++u) {
+        const int row = (qa0 + u) * 8 + lr;
+        const int ch = (lane & 7) ^ ((row >> 1) & 7);
+        const int m = m0 + row;
+        const bool ok = wave_a && m < a.M;
+        const int oy = ok ? m / a.Wo : 0;
+        const int ox = ok ? m - oy * a.Wo : 0;
+        a_ch[u] = ch;
+        a_iy0[u] = ok ? oy * a.stride - a.pad : -(1 << 20);   // never inside the input
+        a_ix0[u] = ox * a.stride - a.pad;
+        // byte offset of the row's first tap (may lie before the buffer)
+        a_off[u] = ok ? ((a_iy0[u] * a.W + a_ix0[u]) * a.Cin_p + ch * 8) * 2 : (int)kOobOffset;
     }
-    bool b_ok[B_CH];
-    const _Float16 *b_row[B_CH];
+    int b_ch[NB];
+    unsigned b_off[NB];
 #pragma unroll
-    for (int i = 0; i < B_CH; ++i) {
-        int n = nb0 + row_base + i * ROW_STEP;
-        b_ok[i] = n < a.N;
-        b_row[i] = wg + (long)(b_ok[i] ? n : 0) * a.K + kc * 8;
+    for (int u = 0; u < NB; ++u) {
+        const int row = (qb0 + u) * 8 + lr;
+        const int ch = (lane & 7) ^ ((row >> 1) & 7);
+        const int n = nb0 + row;
+        b_ch[u] = ch;
+        b_off[u] = !wave_a || kSplit ? (n < a.N ? (unsigned)((long)n * a.K + ch * 8) * 2u : kOobOffset)
+                                     : kOobOffset;
     }
 
     const int kbeg = blockIdx.y * a.kps;
     const int kend = min(a.K, kbeg + a.kps);
-    // filter tap and channel offset of the current K tile (MODE 1)
     int tap_r = 0, tap_s = 0, ci0 = kbeg;
     if (MODE == 1) {
-        int rs = kbeg / a.Cin_p;
+        const int rs = kbeg / a.Cin_p;
         ci0 = kbeg - rs * a.Cin_p;
         tap_r = rs / a.kw;
         tap_s = rs - tap_r * a.kw;
     }
 
-    h8 ra0[A_CH], rb0[B_CH], ra1[A_CH], rb1[B_CH];
-    auto load_tile = [&](int k0, h8 (&ra)[A_CH], h8 (&rb)[B_CH]) {
-        const int k = k0 + kc * 8;
-        const bool kok = k < kend;
+    // loads of the K tile at k0 into stage J (past the K range: zeros)
+    auto issue = [&](int k0, auto J) {
+        const unsigned sb = lds_addr(buf(J));
+        auto load_a = [&]() {
+            // tap (r, s) and channel block: a uniform shift of every A row's
+            // offset; K tiles never straddle taps, so the range test is uniform
+            const int dy = tap_r * a.dil, dx = tap_s * a.dil;
+            const int shift = MODE == 1 ? ((dy * a.W + dx) * a.Cin_p + ci0) * 2 : k0 * 2;
 #pragma unroll
-        for (int i = 0; i < A_CH; ++i) {
-            if (MODE == 0) {
-                bool ok = kok && a_ok[i];
-                ra[i] = ok ? *(const h8 *)(xg + ((long)a_iy0[i] * a.W + a_ix0[i]) * a.Cin_p + k)
-                           : zero_h8();
-            } else {
-                int iy = a_iy0[i] + tap_r * a.dil;
-                int ix = a_ix0[i] + tap_s * a.dil;
-                bool ok = kok && a_ok[i] && iy >= 0 && iy < a.H && ix >= 0 && ix < a.W;
-                ra[i] = ok ? *(const h8 *)(xg + ((long)iy * a.W + ix) * a.Cin_p + ci0 + kc * 8)
-                           : zero_h8();
+            for (int u = 0; u < NA; ++u) {
+                unsigned off;
+                if (MODE == 1) {
+                    const bool ok = k0 < kend && (unsigned)(a_iy0[u] + dy) < (unsigned)a.H &&
+                                    (unsigned)(a_ix0[u] + dx) < (unsigned)a.W;
+                    off = ok ? (unsigned)(a_off[u] + shift) : kOobOffset;
+                } else {
+                    off = k0 + a_ch[u] * 8 < kend ? (unsigned)a_off[u] + (unsigned)shift : kOobOffset;
+                }
+                dma16_to_lds(xr, sb + (unsigned)((qa0 + u) * 8 * 128), off);
             }
-        }
+        };
+        auto load_b = [&]() {
 #pragma unroll
-        for (int i = 0; i < B_CH; ++i)
-            rb[i] = (kok && b_ok[i]) ? *(const h8 *)(b_row[i] + k0) : zero_h8();
+            for (int u = 0; u < NB; ++u)
+                dma16_to_lds(wr, sb + (unsigned)((BM + (qb0 + u) * 8) * 128),
+                             k0 + b_ch[u] * 8 < kend ? b_off[u] + (unsigned)k0 * 2u : kOobOffset);
+        };
+        if constexpr (kSplit) {
+            load_a();
+            load_b();
+        } else {
+            if (wave_a) load_a();
+            else load_b();
+        }
         if (MODE == 1) {
-            ci0 += BK;
+            ci0 += 64;
             if (ci0 >= a.Cin_p) {
                 ci0 = 0;
                 if (++tap_s == a.kw) {
@@ -419,14 +519,6 @@ __global__ __launch_bounds__(WM *WN * 64) void conv_mfma2_kernel(ConvArgs a) {
                 }
             }
         }
-    };
-    auto store_tile = [&](int buf, const h8 (&ra)[A_CH], const h8 (&rb)[B_CH]) {
-#pragma unroll
-        for (int i = 0; i < A_CH; ++i)
-            *(h8 *)(&As[buf][(row_base + i * ROW_STEP) * LDK + kc * 8]) = ra[i];
-#pragma unroll
-        for (int i = 0; i < B_CH; ++i)
-            *(h8 *)(&Bs[buf][(row_base + i * ROW_STEP) * LDK + kc * 8]) = rb[i];
     };
 
     f16v acc[TM][TN];
@@ -438,79 +530,128 @@ __global__ __launch_bounds__(WM *WN * 64) void conv_mfma2_kernel(ConvArgs a) {
             for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
 
     const int lrow = lane & 31;
-    const int lk = (lane >> 5) * 8;
-
-    // Pipeline: tile t is multiplied from LDS while tile t+1 waits in
-    // registers and the global loads of tile t+2 are in flight.
-    auto mma = [&](int buf) {
+    // LDS element offsets of this lane's operand fragments for the group's
+    // 16-wide K steps grp * KPG .. grp * KPG + KPG - 1: chunk kk*2 + lane/32
+    // of row lane % 32 of each 32-row MFMA tile (tiles start at multiples of
+    // 32 rows)
+    int a_rd[KPG][TM], b_rd[KPG][TN];
 #pragma unroll
-        for (int kk = 0; kk < BK; kk += 16) {
-            h8 fa[TM], fb[TN];
+    for (int u = 0; u < KPG; ++u) {
+        const int kk = grp * KPG + u;
+        const int pos = ((kk * 2 + (lane >> 5)) ^ ((lane >> 1) & 7)) * 8;
 #pragma unroll
-            for (int i = 0; i < TM; ++i)
-                fa[i] = *(const h8 *)(&As[buf][(wm * WTM + i * 32 + lrow) * LDK + kk + lk]);
+        for (int i = 0; i < TM; ++i) a_rd[u][i] = (wm * WTM + i * 32 + lrow) * 64 + pos;
 #pragma unroll
-            for (int j = 0; j < TN; ++j)
-                fb[j] = *(const h8 *)(&Bs[buf][(wn * WTN + j * 32 + lrow) * LDK + kk + lk]);
+        for (int j = 0; j < TN; ++j) b_rd[u][j] = BM * 64 + (wn * WTN + j * 32 + lrow) * 64 + pos;
+    }
+    auto compute = [&](auto J) {
+        const _Float16 *sb = buf(J);
+        h8 fa[KPG][TM], fb[KPG][TN];
+#pragma unroll
+        for (int u = 0; u < KPG; ++u) {
+#pragma unroll
+            for (int i = 0; i < TM; ++i) fa[u][i] = *(const h8 *)(sb + a_rd[u][i]);
+#pragma unroll
+            for (int j = 0; j < TN; ++j) fb[u][j] = *(const h8 *)(sb + b_rd[u][j]);
+        }
+#pragma unroll
+        for (int u = 0; u < KPG; ++u)
 #pragma unroll
             for (int i = 0; i < TM; ++i)
 #pragma unroll
                 for (int j = 0; j < TN; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fa[i], fb[j], acc[i][j],
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fa[u][i], fb[u][j], acc[i][j],
                                                                         0, 0, 0);
-        }
     };
-    const int ntiles = (kend - kbeg + BK - 1) / BK;
-    load_tile(kbeg, ra0, rb0);
-    store_tile(0, ra0, rb0);
-    if (ntiles > 1) load_tile(kbeg + BK, ra1, rb1);
-    __syncthreads();
-    // two tiles per trip so that the register sets are named statically
-    for (int t = 0; t < ntiles; t += 2) {
-        // tile t in LDS buffer 0, tile t+1 in ra1/rb1
-        if (t + 2 < ntiles) load_tile(kbeg + (t + 2) * BK, ra0, rb0);
-        mma(0);
-        if (t + 1 < ntiles) store_tile(1, ra1, rb1);
-        __syncthreads();
-        if (t + 1 >= ntiles) break;
-        // tile t+1 in LDS buffer 1, tile t+2 in ra0/rb0
-        if (t + 3 < ntiles) load_tile(kbeg + (t + 3) * BK, ra1, rb1);
-        mma(1);
-        if (t + 2 < ntiles) store_tile(0, ra0, rb0);
-        __syncthreads();
+
+    const int ntiles = (kend - kbeg + 63) / 64;
+    static_for<S - 1>([&](auto J) { issue(kbeg + decltype(J)::value * 64, J); });
+    // one K tile per step: wait for its loads (every wave), barrier (also
+    // frees the stage multiplied in the previous step), refill that stage
+    // with the tile S - 1 ahead, multiply
+    auto step = [&](int u, auto J) {
+        // the memory clobbers keep the previous step's LDS reads above the
+        // wait and the barrier
+        asm volatile("" ::: "memory");
+        wait_vmcnt<(S - 2) * NI>();
+        wait_lgkmcnt0();
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+        issue(kbeg + (u + S - 1) * 64, std::integral_constant<int, decltype(J)::value + S - 1>{});
+        compute(J);
+    };
+    // whole groups of S tiles in the loop (its only exit is the condition,
+    // which keeps the accumulators in place), then the remainder
+    int t = 0;
+    for (; t + S <= ntiles; t += S)
+        static_for<S>([&](auto J) { step(t + decltype(J)::value, J); });
+    const int rem = ntiles - t;
+    static_for<S - 1>([&](auto J) {
+        if (rem > decltype(J)::value) step(t + decltype(J)::value, J);
+    });
+
+    // the loads issued past the end of the K range (zeros) have landed and
+    // every wave is done with the operand stages before the epilogue reuses
+    // them
+    wait_vmcnt<0>();
+
+    // epilogue: 32 rows of the tile at a time through LDS; the K groups'
+    // partial sums are added in group order
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+#pragma unroll
+        for (int wmm = 0; wmm < 2; ++wmm) {
+            __syncthreads();
+            if (wm == wmm) {
+                float *dst = stc + grp * 32 * LDC;
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+#pragma unroll
+                    for (int v = 0; v < 16; ++v)
+                        dst[((v >> 2) * 8 + (lane >> 5) * 4 + (v & 3)) * LDC + wn * WTN + j * 32 + lrow] =
+                            acc[i][j][v];
+            }
+            __syncthreads();
+            const int mb = m0 + wmm * WTM + i * 32;
+            for (int q = tid; q < 32 * BN / 8; q += NT) {
+                const int r = q / (BN / 8), nl = (q % (BN / 8)) * 8;
+                const int m = mb + r, n = nb0 + nl;
+                if (m >= a.M || n >= a.n_cover) continue;
+                float v[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) v[e] = stc[r * LDC + nl + e];
+#pragma unroll
+                for (int g = 1; g < KG; ++g)
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) v[e] += stc[(g * 32 + r) * LDC + nl + e];
+                finish8(a, m, n, v);
+            }
+        }
     }
-    static_assert(BM * (BN + 4) * 4 <= 2 * (BM + BN) * LDK * 2, "staging tile exceeds LDS");
-    if (a.swiglu)
-        conv_epilogue<BM, BN, WM, WN>(a, acc, m0, nb0, lane, wm, wn);
-    else
-        conv_epilogue_lds<BM, BN, WM, WN, NT>(a, acc, (float *)lds, m0, nb0, lane, wm, wn);
 }
 
 struct ConvVariant {
     int bm, bn, bk;
-    int kind;   // 0: conv_mfma general, 1: conv_mfma 1x1, 2: conv_mfma2 1x1, 3: conv_mfma2 aligned
+    int kind;   // 0: conv_mfma (any Cin_p), 4: conv_mfma3 1x1 / token GEMM, 5: conv_mfma3 taps
     const char *name;
     void (*fn)(ConvArgs);
     int threads;
 };
 
-#define SN_CONV_VARIANT(BM, BN, BK, WM, WN, ONE, SUFFIX)                          \
-    {BM, BN, BK, ONE ? 1 : 0, "conv_mfma_" #BM "x" #BN "x" #BK "_w" #WM #WN SUFFIX, \
-     conv_mfma_kernel<BM, BN, BK, WM, WN, ONE>, WM * WN * 64}
-#define SN_CONV_PAIR(BM, BN, BK, WM, WN) \
-    SN_CONV_VARIANT(BM, BN, BK, WM, WN, false, "_gen"), SN_CONV_VARIANT(BM, BN, BK, WM, WN, true, "_1x1")
-#define SN_CONV2_PAIR(BM, BN, WM, WN)                                                        \
-    {BM, BN, 64, 2, "conv2_mfma_" #BM "x" #BN "_w" #WM #WN "_1x1", conv_mfma2_kernel<BM, BN, WM, WN, 0>, \
-     WM * WN * 64},                                                                            \
-    {BM, BN, 64, 3, "conv2_mfma_" #BM "x" #BN "_w" #WM #WN "_tap", conv_mfma2_kernel<BM, BN, WM, WN, 1>, \
-     WM * WN * 64}
+#define SN_CONV_VARIANT(BM, BN, BK, WM, WN)                                              \
+    {BM, BN, BK, 0, "conv_mfma_" #BM "x" #BN "x" #BK "_w" #WM #WN "_gen",                 \
+     conv_mfma_kernel<BM, BN, BK, WM, WN, false>, WM * WN * 64}
+#define SN_CONV3_PAIR(BM, BN, S, KG)                                                          \
+    {BM, BN, 64, 4, "conv3_mfma_" #BM "x" #BN "_s" #S "_g" #KG "_1x1",                        \
+     conv_mfma3_kernel<BM, BN, S, 0, KG>, 256 * KG},                                             \
+    {BM, BN, 64, 5, "conv3_mfma_" #BM "x" #BN "_s" #S "_g" #KG "_tap",                        \
+     conv_mfma3_kernel<BM, BN, S, 1, KG>, 256 * KG}
 
 static const ConvVariant kConvVariants[] = {
-    SN_CONV_PAIR(128, 128, 32, 2, 2), SN_CONV_PAIR(128, 64, 32, 2, 2),
-    SN_CONV_PAIR(64, 128, 32, 2, 2),  SN_CONV_PAIR(64, 64, 32, 2, 2),
-    SN_CONV_PAIR(32, 64, 64, 1, 2),   SN_CONV_PAIR(32, 32, 64, 1, 1),
-    SN_CONV2_PAIR(128, 128, 2, 2),    SN_CONV2_PAIR(128, 64, 2, 2),
-    SN_CONV2_PAIR(64, 128, 2, 2),     SN_CONV2_PAIR(64, 64, 2, 2),
+    SN_CONV_VARIANT(128, 128, 32, 2, 2), SN_CONV_VARIANT(128, 64, 32, 2, 2),
+    SN_CONV_VARIANT(64, 128, 32, 2, 2),  SN_CONV_VARIANT(64, 64, 32, 2, 2),
+    SN_CONV3_PAIR(128, 128, 3, 2),       SN_CONV3_PAIR(64, 128, 4, 2),
+    SN_CONV3_PAIR(64, 64, 4, 2),
 };
 static constexpr int kNumConvVariants = sizeof(kConvVariants) / sizeof(kConvVariants[0]);
 
@@ -578,43 +719,51 @@ static int find_variant(int bm, int bn, int kind) {
 }
 
 // Tile and K split from the whole layer's shape (never from a slab's channel
-// range): the largest 4-wave tile that gives every CU a block; otherwise
-// 64 x 64 tiles with the K range split so that about 256 blocks run, each
-// over at least four K tiles of 32 (two of 64).  1x1 convolutions and taps
-// with Cin_p a multiple of 64 use the double-buffered kernel; the rest (the
-// first layers, Cin_p < 64) the single-buffered one.
+// range), so that every piece of a layer runs the same reduction order.
+// Batch-1 layers have few output tiles: the largest tile that still gives
+// (nearly) every CU a block wins; below that, 64 x 64 tiles, and the K range
+// is split only for long reductions on tiny grids (the partial sums cost a
+// second pass over ksplit x M x N fp32 values).  1x1 convolutions, token
+// GEMMs and taps with Cin_p a multiple of 64 use the multi-stage kernel; the
+// rest (the first layer, Cin_p < 64) the single-buffered general one.
 ConvPlan conv_plan(int M, int N, int K, int cin_p, bool is1x1, bool allow_split) {
     const int target = 256;
-    const int kind = is1x1 ? 2 : (cin_p % 64 == 0 ? 3 : 0);
+    const int kind = is1x1 ? 4 : (cin_p % 64 == 0 ? 5 : 0);
     ConvPlan p;
-    static const int tiles[][2] = {{128, 128}, {128, 64}, {64, 128}, {64, 64}};
+    p.kps = K;
+    if (kind == 0) {
+        static const int tiles[][2] = {{128, 128}, {128, 64}, {64, 128}, {64, 64}};
+        for (auto &t : tiles) {
+            const long blocks = (long)((M + t[0] - 1) / t[0]) * ((N + t[1] - 1) / t[1]);
+            if (blocks >= target - 16) {
+                p.kernel = find_variant(t[0], t[1], kind);
+                return p;
+            }
+        }
+        p.kernel = find_variant(64, 64, kind);
+        return p;
+    }
+    static const int tiles[][2] = {{128, 128}, {64, 128}};
     for (auto &t : tiles) {
-        long blocks = (long)((M + t[0] - 1) / t[0]) * ((N + t[1] - 1) / t[1]);
+        if ((t[0] > 64 && M <= 64) || (t[1] > 64 && N <= 64)) continue;
+        const long blocks = (long)((M + t[0] - 1) / t[0]) * ((N + t[1] - 1) / t[1]);
         if (blocks >= target - 16) {
             p.kernel = find_variant(t[0], t[1], kind);
-            p.kps = K;
             return p;
         }
     }
     p.kernel = find_variant(64, 64, kind);
-    const ConvVariant &v = kConvVariants[p.kernel];
-    long blocks = (long)((M + 63) / 64) * ((N + 63) / 64);
-    const int kt = (K + v.bk - 1) / v.bk;
-    const int min_tiles = v.bk == 64 ? 2 : 4;
-    // the reduction kernel costs about as much as a dozen K tiles of a
-    // latency-bound block: short K ranges are not split
-    const bool long_k = K >= 768;
-    int s = allow_split && long_k ? (int)std::min<long>((target + blocks - 1) / blocks, kt / min_tiles) : 1;
-    if (s < 2) {
-        p.kps = K;
-        return p;
-    }
-    const int per = (kt + s - 1) / s;
-    p.kps = per * v.bk;
-    p.ksplit = (K + p.kps - 1) / p.kps;
-    if (p.ksplit < 2) {
-        p.ksplit = 1;
-        p.kps = K;
+    const long blocks = (long)((M + 63) / 64) * ((N + 63) / 64);
+    const int kt = (K + 63) / 64;
+    if (allow_split && blocks <= 32 && K >= 2304) {
+        const int s = std::min(8, kt / 2);
+        const int per = (kt + s - 1) / s;
+        p.kps = per * 64;
+        p.ksplit = (K + p.kps - 1) / p.kps;
+        if (p.ksplit < 2) {
+            p.ksplit = 1;
+            p.kps = K;
+        }
     }
     return p;
 }
@@ -631,6 +780,9 @@ hipError_t launch_conv(const ConvPlan &p, ConvArgs a, hipStream_t s, hipEvent_t 
     a.ksplit = p.ksplit;
     a.kps = p.ksplit > 1 ? p.kps : a.K;
     if (a.ksplit > 1 && (!a.ws || a.swiglu)) return hipErrorInvalidValue;
+    // buffer-load offsets are 32-bit (kOobOffset marks "outside")
+    if ((long)a.H * a.W * a.Cin_p * 2 >= (long)kOobOffset || (long)a.N * a.K * 2 >= (long)kOobOffset)
+        return hipErrorInvalidValue;
     a.n_cover = std::max(a.N, a.n_zero_end - a.n0);
     long blocks = (long)((a.M + v.bm - 1) / v.bm) * ((a.n_cover + v.bn - 1) / v.bn);
     hipLaunchKernelGGL(v.fn, dim3((unsigned)blocks, (unsigned)a.ksplit), dim3(v.threads), 0, s, a);
@@ -881,8 +1033,6 @@ hipError_t launch_hwc_to_chw(const void *x, void *y, int C, int H, int W, int Cp
 // Swap-in copy kernel: each thread keeps four 16-byte host reads in flight;
 // reads are non-temporal (the image is read once per inference).
 // ---------------------------------------------------------------------------
-typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-
 __global__ __launch_bounds__(256) void swapin_kernel(const u32x4 *__restrict__ src,
                                                      u32x4 *__restrict__ dst, long n16) {
     const long stride = (long)gridDim.x * 256;
