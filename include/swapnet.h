@@ -233,6 +233,13 @@ typedef struct sn_slab_info {
     int32_t wait_slab;          /* this slab's swap-in waits for the compute of
                                    this earlier slab (-1: none), whose arena
                                    range it overwrites                         */
+    int32_t wrap_slab;          /* wait_slab == -1 only: the swap-in of the
+                                   next inference waits for this inference's
+                                   compute of this later slab, the last one
+                                   overlapping its range (-1: none; with
+                                   wait_slab == -1 too, no other slab shares
+                                   the range and the swap-in waits for
+                                   nothing)                                    */
 } sn_slab_info;
 int sn_get_slab(const sn_ctx *ctx, int i, sn_slab_info *out);
 

@@ -59,6 +59,9 @@ struct Slab {
     int64_t image_off = 0, arena_off = 0;
     int wait = -1;                    // newest earlier slab whose arena range this
                                       // slab's swap-in overwrites (-1: none)
+    int wrap = -1;                    // wait == -1: last slab of the inference that
+                                      // overlaps this range; the next inference's
+                                      // swap-in of this slab waits for it (-1: none)
 };
 
 struct PlanResult {

@@ -66,9 +66,19 @@ struct sn_ctx {
     std::condition_variable cv;
     uint64_t requested = 0;            // guarded by mu
     bool stop = false;                 // guarded by mu
-    uint64_t seq = 0;                  // inference sequence number (main thread)
+    uint64_t seq = 0;                  // inference sequence number, any swap-in mode
+    uint64_t tseq = 0;                 // copy-thread inferences (main thread)
     std::atomic<uint64_t> handled{0};  // last inference whose copies were all issued
     std::atomic<uint64_t> fork_seq{0}, abort_seq{0};
+    // last inference whose slabs were all enqueued (an aborted one leaves
+    // work of unknown extent on the compute stream: the next inference's
+    // swap-ins then wait for its start instead of for `wrap` slabs)
+    std::atomic<uint64_t> complete_seq{0};
+    bool prev_threaded = true;         // swap-in mode of inference `seq`
+    // the previous inference was a complete copy-thread one: the copy thread
+    // may start swap-ins that only wait for its `wrap` slabs
+    std::atomic<bool> wrap_ok{false};
+    bool wrap_ok_nt = false;           // same, for swap-ins issued by the calling thread
     std::unique_ptr<std::atomic<uint64_t>[]> loaded_seq;
     // completion counters written by the compute stream (signal kernels) in
     // pinned host memory: [0, ns) per slab, ns = inference start
@@ -566,9 +576,17 @@ static void copier_main(sn_ctx *c) {
             // queue's per-copy start-up overlaps the other's transfer
             hipStream_t q = (c->copy_streams == 2 && (i & 1)) ? c->copy_s2 : c->copy_s;
             // the compute this slab's DMA must follow has completed once its
-            // counter reaches `seq` (no runtime call while waiting)
-            volatile unsigned long long *gate = c->sig_host + (s.wait >= 0 ? s.wait : ns);
-            while (*gate < seq) {
+            // counter reaches `need` (no runtime call while waiting): slab
+            // `wait` of this inference, else slab `wrap` of the previous one,
+            // else the start of this inference
+            // (a range no other slab shares is rewritten with the same bytes:
+            // no wait at all)
+            const bool wrap = s.wait < 0 && s.wrap >= 0 && c->wrap_ok.load();
+            const bool exclusive = s.wait < 0 && s.wrap < 0;
+            const int gi = s.wait >= 0 ? s.wait : (wrap ? s.wrap : ns);
+            const uint64_t need = exclusive ? 0 : (wrap ? seq - 1 : seq);
+            volatile unsigned long long *gate = c->sig_host + gi;
+            while (*gate < need) {
                 if (c->abort_seq.load() >= seq) {
                     aborted = true;
                     break;
@@ -597,7 +615,7 @@ static void copier_main(sn_ctx *c) {
 
 static void wait_copier_idle(sn_ctx *c) {
     if (!c->copier.joinable()) return;
-    while (c->handled.load() < c->seq) cpu_relax();
+    while (c->handled.load() < c->tseq) cpu_relax();
 }
 
 static void start_copier(sn_ctx *c) {
@@ -619,11 +637,17 @@ static void stop_copier(sn_ctx *c) {
 
 // Swap-in of slab i on the copy stream.  It overwrites arena bytes last used
 // by slab `wait` (the newest earlier slab overlapping its range), so it waits
-// for that slab's compute; a slab with no such predecessor waits only for
-// the start of the inference, which follows the previous inference.
+// for that slab's compute; a slab with no such predecessor waits for the
+// previous inference's compute of slab `wrap` (the last slab sharing its
+// range; an event never recorded, before the first inference, does not
+// hold the copy), or else for the start of the inference.  A range that no
+// other slab shares only ever receives the same bytes: no wait.
 static int enqueue_copy(sn_ctx *c, int i) {
     const Slab &s = c->plan.slabs[i];
-    HIP_TRY(c, hipStreamWaitEvent(c->copy_s, s.wait >= 0 ? c->done[s.wait] : c->fork, 0));
+    const bool wrap = s.wait < 0 && s.wrap >= 0 && c->wrap_ok_nt;
+    const bool exclusive = s.wait < 0 && s.wrap < 0;   // range shared with no other slab
+    hipEvent_t ev = s.wait >= 0 ? c->done[s.wait] : (wrap ? c->done[s.wrap] : c->fork);
+    if (!exclusive) HIP_TRY(c, hipStreamWaitEvent(c->copy_s, ev, 0));
     if (c->timing) HIP_TRY(c, hipEventRecord(c->t_in0[i], c->copy_s));
     if (s.bytes) {
         if (c->swapin != 0)
@@ -660,13 +684,19 @@ static int run_slabs(sn_ctx *c, int n_tok, hipStream_t cs, Pre pre, Post post, b
     const bool threaded = swap && c->swapin == 2;
     int rc;
     uint64_t seq = 0;
+    // may the swap-ins wait for the previous inference's `wrap` slabs?
+    const bool prev_complete = c->complete_seq.load() == c->seq;
+    c->wrap_ok_nt = prev_complete;
+    const uint64_t run = ++c->seq;
     if (threaded) {
         // the copy thread must be done with the previous inference's events
         // before they are recorded again
         wait_copier_idle(c);
         if (c->copy_error.exchange(0)) return fail(c, SN_E_HIP, c->copy_err);
-        seq = ++c->seq;
+        seq = ++c->tseq;
+        c->wrap_ok.store(prev_complete && c->prev_threaded);
     }
+    c->prev_threaded = threaded;
     auto abort_copies = [&](int r) {
         if (threaded) c->abort_seq.store(seq);
         return r;
@@ -720,6 +750,7 @@ static int run_slabs(sn_ctx *c, int n_tok, hipStream_t cs, Pre pre, Post post, b
         if (e != hipSuccess) return abort_copies(fail(c, SN_E_HIP, hipGetErrorString(e)));
         if (!threaded && (rc = issue(i))) return rc;
     }
+    c->complete_seq.store(run);
     return SN_OK;
 }
 
@@ -958,6 +989,7 @@ extern "C" int sn_get_slab(const sn_ctx *c, int i, sn_slab_info *o) {
     o->bytes = s.bytes;
     o->first_piece = s.pieces.empty() ? -1 : s.pieces.front();
     o->wait_slab = s.wait;
+    o->wrap_slab = s.wrap;
     o->n_pieces = (int32_t)s.pieces.size();
     if (i < (int)c->slab_t_in.size()) {
         o->t_in_ms = c->slab_t_in[i];

@@ -515,6 +515,7 @@ int place_slabs(PlanResult &p, int64_t arena_budget, std::string &err) {
         const int64_t next = i + 1 < n ? p.slabs[i + 1].bytes : 0;
         int best_wait = 1 << 30;
         int64_t best_off = -1;
+        bool best_clear0 = false;
         for (int64_t c : cand) {
             if (c < 0 || c + s.bytes > B || c % kAlign) continue;
             if (i > 0 && overlap(c, s.bytes, p.slabs[i - 1].arena_off, p.slabs[i - 1].bytes)) continue;
@@ -526,9 +527,14 @@ int place_slabs(PlanResult &p, int64_t arena_budget, std::string &err) {
                     w = j;
                     break;
                 }
-            if (w < best_wait || (w == best_wait && c < best_off)) {
+            // ties: keep clear of slab 0's range (the next inference's first
+            // swap-in then need not wait for this slab), then the lowest offset
+            const bool clear0 = i == 0 || !overlap(c, s.bytes, p.slabs[0].arena_off, p.slabs[0].bytes);
+            if (w < best_wait || (w == best_wait && clear0 && !best_clear0) ||
+                (w == best_wait && clear0 == best_clear0 && c < best_off)) {
                 best_wait = w;
                 best_off = c;
+                best_clear0 = clear0;
             }
         }
         if (best_off < 0) {
@@ -538,6 +544,20 @@ int place_slabs(PlanResult &p, int64_t arena_budget, std::string &err) {
         s.arena_off = best_off;
         s.wait = best_wait;
         p.high_water = std::max(p.high_water, s.arena_off + s.bytes);
+    }
+    // Back-to-back inferences: a slab whose range no earlier slab of the same
+    // inference uses is overwritten, one inference later, only after the last
+    // slab that shares its range has run, so its swap-in can start while the
+    // previous inference is still computing its remaining slabs.
+    for (int j = 0; j < n; ++j) {
+        Slab &s = p.slabs[j];
+        s.wrap = -1;
+        if (s.wait >= 0) continue;
+        for (int i = n - 1; i > j; --i)
+            if (overlap(s.arena_off, s.bytes, p.slabs[i].arena_off, p.slabs[i].bytes)) {
+                s.wrap = i;
+                break;
+            }
     }
     return SN_OK;
 }

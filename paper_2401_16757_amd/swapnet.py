@@ -60,7 +60,7 @@ class SnSlabInfo(C.Structure):
                 ("first_piece", C.c_int32), ("n_pieces", C.c_int32),
                 ("t_in_ms", C.c_float), ("t_ex_ms", C.c_float),
                 ("t_in_start_ms", C.c_float), ("t_ex_start_ms", C.c_float),
-                ("wait_slab", C.c_int32)]
+                ("wait_slab", C.c_int32), ("wrap_slab", C.c_int32)]
 
 
 class SnPieceInfo(C.Structure):

@@ -152,6 +152,34 @@ def test_infer_dev_on_torch_stream_matches_host_path():
         assert np.array_equal(yd.cpu().numpy().view(np.uint16), y_host.view(np.uint16))
 
 
+@pytest.mark.parametrize("modes", [(2,), (1,), (0,), (2, 1, 0, 2)])
+def test_back_to_back_inferences_with_cross_inference_prefetch(modes):
+    # Several inferences queued without a host synchronisation: the next
+    # inference's swap-ins of slabs that no earlier slab shares start while
+    # the previous one still computes (waiting only for its `wrap` slabs).
+    # Every output must equal a one-at-a-time inference of the same input,
+    # bit for bit, in every swap-in mode and when the modes alternate.
+    net, wts, x0, _ = net_case("resnet50", res=96)
+    rng = np.random.default_rng(7)
+    xs = [x0] + [rng.standard_normal(x0.shape).astype(np.float16) for _ in range(3)]
+    with S.build_engine(net, wts) as eng:
+        assert eng.stats()["n_slabs"] >= 4 and not eng.stats()["resident"]
+        assert any(s["wrap_slab"] >= 0 for s in eng.slabs())
+        want = [eng.infer(x) for x in xs]
+        xd = [torch.from_numpy(x).cuda() for x in xs]
+        s = torch.cuda.Stream()
+        for mode in modes:
+            eng.set_option(S.OPT_SWAPIN, mode)
+            yd = [torch.empty(eng.out_shape, dtype=torch.float16, device="cuda") for _ in xs]
+            with torch.cuda.stream(s):
+                for rep in range(2):
+                    for i in range(len(xs)):
+                        eng.infer_dev(xd[i].data_ptr(), yd[i].data_ptr(), s.cuda_stream)
+            s.synchronize()
+            for i in range(len(xs)):
+                assert np.array_equal(yd[i].cpu().numpy().view(np.uint16), want[i].view(np.uint16)), (mode, i)
+
+
 def small_decoder(**kw):
     a = dict(n_layers=2, d=128, heads=4, ffn=160, vocab=300, max_seq=48, prompt=24, gen=8)
     a.update(kw)

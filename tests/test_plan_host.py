@@ -89,6 +89,14 @@ def check_plan(net, eng, budget):
                 t = slabs[w]
                 assert not (s["arena_off"] + s["bytes"] <= t["arena_off"] or
                             t["arena_off"] + t["bytes"] <= s["arena_off"])
+            # the next inference's swap-in of a slab without an earlier
+            # overlapping slab waits for the last overlapping slab of this one
+            def over(u, v):
+                return not (u["arena_off"] + u["bytes"] <= v["arena_off"] or
+                            v["arena_off"] + v["bytes"] <= u["arena_off"])
+            later = [j for j in range(i + 1, len(slabs)) if over(s, slabs[j])]
+            expect = (later[-1] if later else -1) if w == -1 else -1
+            assert s["wrap_slab"] == expect, (i, s["wrap_slab"], expect)
     assert total == st["image_bytes"]
     # streamed bytes: the weights plus alignment padding only
     assert st["image_bytes"] >= net.streamed_weight_bytes()
