@@ -50,6 +50,10 @@ def parse():
     ap.add_argument("--no-graph", action="store_true", help="enqueue call by call (no HIP graph)")
     ap.add_argument("--swapin", type=int, default=2, choices=[0, 1, 2],
                     help="0 copy kernel, 1 SDMA from the calling thread, 2 SDMA from the copy thread")
+    ap.add_argument("--copy-streams", type=int, default=1, choices=[1, 2],
+                    help="DMA queues used by the copy thread (consecutive slabs alternate)")
+    ap.add_argument("--swapin-blocks", type=int, default=None,
+                    help="workgroups of the copy kernel (--swapin 0)")
     ap.add_argument("--pmc-calibration", action="store_true",
                     help="also run one 256 MiB device-to-device copy (counter calibration)")
     return ap.parse_args()
@@ -81,6 +85,35 @@ def measure_h2d_peak(torch, sizes=(64 << 20, 256 << 20), reps=8):
             e1.synchronize()
             rates.append(n / (e0.elapsed_time(e1) * 1e-3) / 1e9)
         best = max(best, float(np.median(rates)))
+    del h, d
+    return best
+
+
+def measure_copy_chain(torch, sizes, reps=5):
+    """Time (ms) of the swap-in copies alone: one pinned host -> device copy
+    per slab, back to back on one stream with an event after each (as the
+    engine issues them), no compute.  The floor that per-copy DMA start-up
+    puts on a swapped inference with this many slabs."""
+    total = sum(sizes)
+    h = torch.empty(total, dtype=torch.uint8, pin_memory=True)
+    h.fill_(1)
+    d = torch.empty(total, dtype=torch.uint8, device="cuda")
+    s = torch.cuda.Stream()
+    evs = [torch.cuda.Event() for _ in sizes]
+    best = None
+    with torch.cuda.stream(s):
+        for _ in range(reps + 1):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(s)
+            off = 0
+            for n, ev in zip(sizes, evs):
+                d[off:off + n].copy_(h[off:off + n], non_blocking=True)
+                ev.record(s)
+                off += n
+            e1.record(s)
+            e1.synchronize()
+            t = e0.elapsed_time(e1)
+            best = t if best is None else min(best, t)
     del h, d
     return best
 
@@ -176,8 +209,12 @@ def kernel_profile(S, net, eng, torch, xd, yd):
         if spec.op == "conv2d":
             ho, wo = spec.out_hw()
             m, n = ho * wo, p["c1"] - p["c0"]
+            # algorithmic bytes: input activation, weights, bias, output (and
+            # residual) once each
+            cin_p = (spec.c_in + 7) // 8 * 8
+            act = spec.h_in * spec.w_in * cin_p * 2 + m * n * 2 * (2 if spec.res >= 0 else 1)
             add(S.kernel_name(p["kernel"]), p["t_main_ms"], conv_flops(spec, p["c0"], p["c1"]),
-                p["w_bytes"] + p["b_bytes"])
+                p["w_bytes"] + p["b_bytes"] + act)
             if p["ksplit"] > 1:
                 add("splitk_reduce", p["t_ms"] - p["t_main_ms"], 0.0,
                     4.0 * p["ksplit"] * m * n + 2.0 * m * n)
@@ -343,6 +380,9 @@ def main():
     st = eng_sw.stats()
     eng_res = S.build_engine(net, wts, budget=st["image_bytes"] + 4096)
     eng_sw.set_option(S.OPT_SWAPIN, a.swapin)
+    eng_sw.set_option(S.OPT_COPY_STREAMS, a.copy_streams)
+    if a.swapin_blocks:
+        eng_sw.set_option(S.OPT_SWAPIN_BLOCKS, a.swapin_blocks)
     if a.no_graph:
         eng_sw.set_option(S.OPT_GRAPH, 0)
         eng_res.set_option(S.OPT_GRAPH, 0)
@@ -376,6 +416,8 @@ def main():
 
     streamed = st["streamed_bytes"]
     h2d = streamed / (sw_ms * 1e-3) / 1e9
+    log("timing the swap-in copies alone")
+    chain_ms = measure_copy_chain(torch, [sl["bytes"] for sl in eng_sw.slabs()])
     log("timeline and kernel profile (untimed passes)")
     tl = slab_timeline(S, eng_sw, x)
     groups = kernel_profile(S, net, eng_res, torch, xd, yr)
@@ -385,12 +427,19 @@ def main():
     res_compute_ms = sum(v[1] for v in groups.values())
     roofline = None
     if dom:
-        name, (launches, tms, fl, _) = dom
-        ach = fl / (tms * 1e-3) / 1e12
-        roofline = {"bound": "mfma", "kernel": name, "launches_per_step": launches,
+        # the kernel's bound: MFMA if its FLOPs take longer at peak than its
+        # algorithmic bytes at HBM peak, else HBM (batch-1 layers mostly are)
+        name, (launches, tms, fl, by) = dom
+        if fl / (MFMA_FP16_PEAK_TFLOPS * 1e12) >= by / (HBM_PEAK_GBS * 1e9):
+            ach, peak_r, unit, bound = fl / (tms * 1e-3) / 1e12, MFMA_FP16_PEAK_TFLOPS, "TFLOP/s", "mfma"
+        else:
+            ach, peak_r, unit, bound = by / (tms * 1e-3) / 1e9, HBM_PEAK_GBS, "GB/s", "hbm"
+        roofline = {"bound": bound, "kernel": name, "launches_per_step": launches,
                     "avg_launch_us": round(tms / launches * 1e3, 3),
-                    "achieved": round(ach, 2), "peak": MFMA_FP16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                    "frac": round(ach / MFMA_FP16_PEAK_TFLOPS, 5),
+                    "achieved": round(ach, 2), "peak": peak_r, "unit": unit,
+                    "frac": round(ach / peak_r, 5),
+                    "flops_per_launch": round(fl / launches), "bytes_per_launch": round(by / launches),
+                    "mfma_tflops": round(fl / (tms * 1e-3) / 1e12, 2),
                     "traffic": recorded_traffic(name) if a.workload == "resnet50" else None}
     mfma_util = (total_flops / (res_compute_ms * 1e-3) / 1e12) / MFMA_FP16_PEAK_TFLOPS \
         if res_compute_ms > 0 else None
@@ -420,7 +469,9 @@ def main():
         "h2d_frac": round(h2d / peak, 4),
         "link": {"bound": "pcie_h2d", "achieved": round(h2d, 2), "peak": round(peak, 2),
                  "unit": "GB/s", "frac": round(h2d / peak, 4),
-                 "traffic": streamed},
+                 "traffic": streamed,
+                 "copy_chain_ms": round(chain_ms, 4),
+                 "swapped_vs_copy_chain": round(chain_ms / sw_ms, 4)},
         "link_floor_ms": round(streamed / (peak * 1e9) * 1e3, 4),
         "mfma_util": round(mfma_util, 5) if mfma_util else None,
         "roofline": roofline,

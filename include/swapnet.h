@@ -77,7 +77,9 @@ enum sn_op {
     SN_OP_RMSNORM = 7,          /* gain [c_in]: v / sqrt(mean(v^2)+eps) * g    */
     SN_OP_ATTENTION = 8         /* src = [T][3d] (q|k|v); RoPE (rotate-half,
                                    theta), append k, v to the KV cache of
-                                   kv_layer, causal softmax(q k^T/sqrt(hd)) v  */
+                                   kv_layer, causal softmax(q k^T/sqrt(hd)) v;
+                                   head_dim a power of two in [8, 512]
+                                   (else SN_E_UNSUPPORTED at sn_add_block)     */
 };
 
 /* Layer flags. */
@@ -219,6 +221,10 @@ typedef struct sn_stats {
     int32_t n_slabs, n_pieces, n_layers, resident;
     int64_t n_infers;
     double last_ms;             /* last inference, host wall clock (ms)       */
+    int64_t input_bytes;        /* bytes sn_infer reads from `input` (0 for
+                                   token networks)                             */
+    int64_t output_bytes;       /* bytes sn_infer / sn_infer_tokens write to
+                                   `output` / `logits`                         */
 } sn_stats;
 int sn_get_stats(const sn_ctx *ctx, sn_stats *out);
 

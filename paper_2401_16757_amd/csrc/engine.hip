@@ -89,11 +89,13 @@ struct sn_ctx {
     int64_t act_bytes = 0;
     uint8_t *kv = nullptr;
     int64_t kv_bytes = 0;
+    int64_t attn_ws_bytes = 0;
     int kv_layers = 0, max_seq = 0, d_model = 0, max_tokens = 0;
     void *table_host = nullptr, *table_dev = nullptr;
     int64_t table_bytes = 0;
     int32_t *d_ids = nullptr;
     float *q_scratch = nullptr;
+    float *attn_ws = nullptr;          // per-chunk attention partials (decode)
     void *in_stage = nullptr, *out_stage = nullptr;
     float *ws = nullptr;               // split-K partial sums (outside the budget)
     int64_t ws_bytes = 0;
@@ -335,6 +337,11 @@ extern "C" int sn_plan(sn_ctx *c) {
         HIP_TRY(c, hipMalloc((void **)&c->kv, (size_t)std::max<int64_t>(c->kv_bytes, kAlign)));
         HIP_TRY(c, hipMalloc((void **)&c->d_ids, (size_t)c->max_tokens * 4));
         HIP_TRY(c, hipMalloc((void **)&c->q_scratch, (size_t)c->max_tokens * c->d_model * 4));
+        int max_hd = 8;
+        for (const Layer &Ly : c->layers)
+            if (Ly.d.op == SN_OP_ATTENTION) max_hd = std::max(max_hd, Ly.d.head_dim);
+        c->attn_ws_bytes = attention_workspace_floats(max_hd) * 4;
+        HIP_TRY(c, hipMalloc((void **)&c->attn_ws, (size_t)c->attn_ws_bytes));
     } else {
         HIP_TRY(c, hipMalloc(&c->in_stage, (size_t)c->in_bytes));
     }
@@ -524,7 +531,7 @@ static int run_piece(sn_ctx *c, int pi, int n_tok, hipStream_t s) {
         const int64_t per = (int64_t)c->max_seq * c->d_model * 2;
         uint8_t *kc = c->kv + (int64_t)d.kv_layer * 2 * per;
         e = launch_attention(slot_ptr(c, d.src), kc, kc + per, c->q_scratch, slot_ptr(c, d.dst),
-                             n_tok, c->pos, d.heads, d.head_dim, d.theta, s);
+                             c->attn_ws, n_tok, c->pos, d.heads, d.head_dim, d.theta, s);
         break;
     }
     default:
@@ -966,10 +973,12 @@ extern "C" int sn_get_stats(const sn_ctx *c, sn_stats *o) {
     o->image_bytes = c->plan.image_bytes;
     o->arena_high_water = c->plan.high_water;
     o->streamed_bytes = c->plan.resident ? 0 : c->plan.image_bytes;
-    o->activation_bytes = c->act_bytes + c->ws_bytes;
+    o->activation_bytes = c->act_bytes + c->ws_bytes + c->attn_ws_bytes;
     o->kv_bytes = c->kv_bytes;
     o->table_bytes = (int64_t)(c->plan.pieces.size() * sizeof(Piece) + c->plan.slabs.size() * sizeof(Slab) +
                                c->piece_w.size() * 2 * sizeof(void *) + c->layers.size() * sizeof(Layer));
+    o->input_bytes = c->token ? 0 : c->in_bytes;
+    o->output_bytes = c->out_bytes;
     o->n_slabs = (int32_t)c->plan.slabs.size();
     o->n_pieces = (int32_t)c->plan.pieces.size();
     o->resident = c->plan.resident ? 1 : 0;
@@ -1053,7 +1062,8 @@ extern "C" void sn_destroy(sn_ctx *c) {
         if (c->table_host) hipHostFree(c->table_host);
         if (c->sig_host) hipHostFree(c->sig_host);
         for (void *p : {(void *)c->arena, (void *)c->act, (void *)c->kv, (void *)c->d_ids,
-                        (void *)c->q_scratch, c->in_stage, c->out_stage, (void *)c->ws})
+                        (void *)c->q_scratch, (void *)c->attn_ws, c->in_stage, c->out_stage,
+                        (void *)c->ws})
             if (p) hipFree(p);
         if (c->copy_s) hipStreamDestroy(c->copy_s);
         if (c->copy_s2) hipStreamDestroy(c->copy_s2);

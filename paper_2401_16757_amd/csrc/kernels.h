@@ -97,9 +97,14 @@ hipError_t launch_embed(const int32_t *ids, const void *table, void *y, int T, i
 hipError_t launch_rmsnorm(const void *x, const void *gain, void *y, int T, int d, float eps,
                           hipStream_t s);
 // RoPE on q and k of each token, append k, v to the cache at pos0 + t, then
-// causal attention of every query over cache positions 0 .. pos0 + t.
+// causal attention of every query over cache positions 0 .. pos0 + t.  `ws`
+// (attention_workspace_floats(head_dim) floats, or null) holds per-chunk
+// partial results when few tokens are processed (decode): the keys are then
+// split over several blocks and merged in a fixed order.
+constexpr int kAttnWsRecords = 512;
+int64_t attention_workspace_floats(int head_dim);
 hipError_t launch_attention(const void *qkv, void *kcache, void *vcache, void *q_scratch,
-                            void *out, int T, int pos0, int heads, int head_dim, float theta,
-                            hipStream_t s);
+                            void *out, float *ws, int T, int pos0, int heads, int head_dim,
+                            float theta, hipStream_t s);
 
 }  // namespace sn

@@ -795,14 +795,15 @@ hipError_t launch_conv(const ConvPlan &p, ConvArgs a, hipStream_t s, hipEvent_t 
 }
 
 // ---------------------------------------------------------------------------
-// GEMV (batch-1 linear).  The input vector is staged in LDS once per block;
-// each wave streams ROWS weight rows with 16-byte loads, four chunks in
-// flight per row, accumulating in fp32 in a fixed order, then reduces across
-// the 64 lanes with a fixed butterfly.
+// GEMV (batch-1 linear), HBM-bound: every weight byte is read once.  Each
+// wave owns ROWS consecutive weight rows and walks K in steps of 64 x U
+// 16-byte chunks: ROWS x U non-temporal weight loads are issued before any
+// of them is used (16 KB in flight per wave), the matching input chunks come
+// from L1/L2 (the vector is shared by every wave), products are accumulated
+// in fp32 in a fixed order, and a fixed butterfly reduces the 64 lanes.
 // ---------------------------------------------------------------------------
-template <int ROWS>
+template <int ROWS, int U>
 __global__ __launch_bounds__(256) void gemv_kernel(GemvArgs a) {
-    extern __shared__ h8 xs[];
     const int tid = threadIdx.x;
     const int kch = a.K / 8;
     if (blockIdx.x == 0 && a.zero_end > 0) {
@@ -812,52 +813,48 @@ __global__ __launch_bounds__(256) void gemv_kernel(GemvArgs a) {
             else ((_Float16 *)a.y)[n] = (_Float16)0.0f;
         }
     }
-    const h8 *xg = (const h8 *)a.x;
-    for (int c = tid; c < kch; c += 256) xs[c] = xg[c];
-    __syncthreads();
-
     const int lane = tid & 63;
     const int wave = tid >> 6;
     const int row0 = (blockIdx.x * 4 + wave) * ROWS;
     if (row0 >= a.rows) return;
-    const h8 *wg = (const h8 *)a.w;
+    const h8 *xg = (const h8 *)a.x;
+    const h8 *wrow[ROWS];
+#pragma unroll
+    for (int r = 0; r < ROWS; ++r)
+        wrow[r] = (const h8 *)a.w + (long)min(row0 + r, a.rows - 1) * kch;   // clamped: never out of range
 
     float acc[ROWS];
 #pragma unroll
     for (int r = 0; r < ROWS; ++r) acc[r] = 0.0f;
 
     int c = lane;
-    for (; c + 192 < kch; c += 256) {
-        h8 xv0 = xs[c], xv1 = xs[c + 64], xv2 = xs[c + 128], xv3 = xs[c + 192];
+    for (; c + 64 * (U - 1) < kch; c += 64 * U) {
+        h8 wv[ROWS][U], xv[U];
+#pragma unroll
+        for (int r = 0; r < ROWS; ++r)
+#pragma unroll
+            for (int u = 0; u < U; ++u) wv[r][u] = __builtin_nontemporal_load(wrow[r] + c + 64 * u);
+#pragma unroll
+        for (int u = 0; u < U; ++u) xv[u] = xg[c + 64 * u];
 #pragma unroll
         for (int r = 0; r < ROWS; ++r) {
-            if (row0 + r < a.rows) {
-                const h8 *wr = wg + (long)(row0 + r) * kch;
-                h8 w0 = wr[c], w1 = wr[c + 64], w2 = wr[c + 128], w3 = wr[c + 192];
-                float s = acc[r];
+            float sacc = acc[r];
 #pragma unroll
-                for (int i = 0; i < 8; ++i) s = fmaf((float)w0[i], (float)xv0[i], s);
+            for (int u = 0; u < U; ++u)
 #pragma unroll
-                for (int i = 0; i < 8; ++i) s = fmaf((float)w1[i], (float)xv1[i], s);
-#pragma unroll
-                for (int i = 0; i < 8; ++i) s = fmaf((float)w2[i], (float)xv2[i], s);
-#pragma unroll
-                for (int i = 0; i < 8; ++i) s = fmaf((float)w3[i], (float)xv3[i], s);
-                acc[r] = s;
-            }
+                for (int i = 0; i < 8; ++i) sacc = fmaf((float)wv[r][u][i], (float)xv[u][i], sacc);
+            acc[r] = sacc;
         }
     }
     for (; c < kch; c += 64) {
-        h8 xv = xs[c];
+        const h8 xv = xg[c];
 #pragma unroll
         for (int r = 0; r < ROWS; ++r) {
-            if (row0 + r < a.rows) {
-                h8 wv = wg[(long)(row0 + r) * kch + c];
-                float s = acc[r];
+            const h8 wv = __builtin_nontemporal_load(wrow[r] + c);
+            float sacc = acc[r];
 #pragma unroll
-                for (int i = 0; i < 8; ++i) s = fmaf((float)wv[i], (float)xv[i], s);
-                acc[r] = s;
-            }
+            for (int i = 0; i < 8; ++i) sacc = fmaf((float)wv[i], (float)xv[i], sacc);
+            acc[r] = sacc;
         }
     }
 #pragma unroll
@@ -900,10 +897,10 @@ __global__ __launch_bounds__(256) void gemv_kernel(GemvArgs a) {
 hipError_t launch_gemv(const GemvArgs &a, hipStream_t s) {
     if (a.rows <= 0) return hipSuccess;
     if (a.K % 8) return hipErrorInvalidValue;
-    constexpr int ROWS = 2;   // even, so SwiGLU pairs stay in one wave
+    constexpr int ROWS = 4;   // even, so SwiGLU pairs stay in one wave
+    constexpr int U = 4;
     unsigned blocks = (unsigned)((a.rows + 4 * ROWS - 1) / (4 * ROWS));
-    size_t lds = (size_t)a.K * 2;
-    hipLaunchKernelGGL(gemv_kernel<ROWS>, dim3(blocks), dim3(256), lds, s, a);
+    hipLaunchKernelGGL((gemv_kernel<ROWS, U>), dim3(blocks), dim3(256), 0, s, a);
     return hipGetLastError();
 }
 
@@ -1102,19 +1099,41 @@ __device__ float block_sum_256(float v, float *red) {
     return (red[0] + red[1]) + (red[2] + red[3]);
 }
 
+// One block per token; 8 channels per thread with 16-byte accesses when d is
+// a multiple of 8.  Sum of squares in a fixed order (per-thread strided
+// partials, then the block reduction).
 __global__ __launch_bounds__(256) void rmsnorm_kernel(const _Float16 *x, const _Float16 *g,
                                                       _Float16 *y, int d, float eps) {
     __shared__ float red[4];
     const _Float16 *xr = x + (long)blockIdx.x * d;
+    _Float16 *yr = y + (long)blockIdx.x * d;
+    const bool vec = (d % 8) == 0;
     float s = 0.0f;
-    for (int c = threadIdx.x; c < d; c += 256) {
-        float v = (float)xr[c];
-        s = fmaf(v, v, s);
+    if (vec) {
+        for (int c = threadIdx.x; c < d / 8; c += 256) {
+            const h8 v = *(const h8 *)(xr + 8 * c);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) s = fmaf((float)v[e], (float)v[e], s);
+        }
+    } else {
+        for (int c = threadIdx.x; c < d; c += 256) {
+            float v = (float)xr[c];
+            s = fmaf(v, v, s);
+        }
     }
     s = block_sum_256(s, red);
-    float scale = 1.0f / sqrtf(s / (float)d + eps);
-    _Float16 *yr = y + (long)blockIdx.x * d;
-    for (int c = threadIdx.x; c < d; c += 256) yr[c] = (_Float16)((float)xr[c] * scale * (float)g[c]);
+    const float scale = 1.0f / sqrtf(s / (float)d + eps);
+    if (vec) {
+        for (int c = threadIdx.x; c < d / 8; c += 256) {
+            const h8 v = *(const h8 *)(xr + 8 * c), gv = *(const h8 *)(g + 8 * c);
+            h8 o;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) o[e] = (_Float16)((float)v[e] * scale * (float)gv[e]);
+            *(h8 *)(yr + 8 * c) = o;
+        }
+    } else {
+        for (int c = threadIdx.x; c < d; c += 256) yr[c] = (_Float16)((float)xr[c] * scale * (float)g[c]);
+    }
 }
 
 hipError_t launch_rmsnorm(const void *x, const void *gain, void *y, int T, int d, float eps,
@@ -1125,23 +1144,32 @@ hipError_t launch_rmsnorm(const void *x, const void *gain, void *y, int T, int d
 }
 
 // RoPE (rotate-half) on q and k; q goes to q_scratch (fp32), k and v to the
-// cache at position pos0 + t.  One block per token, one thread per pair.
+// cache at position pos0 + t.  One block per token.  The rotation angle of
+// pair i at position p is p * theta^(-2i/hd), evaluated once per pair index
+// in double precision (shared by all heads), its cosine and sine rounded to
+// fp32.
 __global__ void rope_append_kernel(const _Float16 *qkv, float *qs, _Float16 *kc, _Float16 *vc,
                                    int pos0, int heads, int hd, float theta) {
+    extern __shared__ float cs_sn[];   // [half] cosines, then [half] sines
     const int t = blockIdx.x;
     const int d = heads * hd;
     const int half = hd / 2;
     const _Float16 *row = qkv + (long)t * 3 * d;
     const long pos = pos0 + t;
+    for (int i = threadIdx.x; i < half; i += blockDim.x) {
+        const double ang = (double)pos * pow((double)theta, -2.0 * (double)i / (double)hd);
+        cs_sn[i] = (float)cos(ang);
+        cs_sn[half + i] = (float)sin(ang);
+    }
+    __syncthreads();
     for (int p = threadIdx.x; p < heads * half; p += blockDim.x) {
-        int h = p / half, i = p - (p / half) * half;
-        double ang = (double)pos * pow((double)theta, -2.0 * (double)i / (double)hd);
-        float cs = (float)cos(ang), sn = (float)sin(ang);
-        int a = h * hd + i, b = a + half;
-        float qa = (float)row[a], qb = (float)row[b];
+        const int h = p / half, i = p - h * half;
+        const float cs = cs_sn[i], sn = cs_sn[half + i];
+        const int a = h * hd + i, b = a + half;
+        const float qa = (float)row[a], qb = (float)row[b];
         qs[(long)t * d + a] = qa * cs - qb * sn;
         qs[(long)t * d + b] = qb * cs + qa * sn;
-        float ka = (float)row[d + a], kb = (float)row[d + b];
+        const float ka = (float)row[d + a], kb = (float)row[d + b];
         kc[pos * d + a] = (_Float16)(ka * cs - kb * sn);
         kc[pos * d + b] = (_Float16)(kb * cs + ka * sn);
         vc[pos * d + a] = row[2 * d + a];
@@ -1149,28 +1177,62 @@ __global__ void rope_append_kernel(const _Float16 *qkv, float *qs, _Float16 *kc,
     }
 }
 
-// One block per (token, head): scores over cache positions 0..pos0+t in LDS,
-// fixed-order max / sum reductions, then each thread owns one output dim and
-// accumulates over positions in order.
+// Causal attention for head_dim a power of two in [8, 512].  A key row
+// (head_dim fp16) is read by LPK = head_dim/8 lanes with one 16-byte load
+// each, so a block covers 256/LPK keys per step with coalesced loads.
+// Scores go to LDS; max and sum are block reductions in a fixed order; for
+// P.V every LPK-lane group accumulates its keys (group, group + G, ...) in
+// order and the G partial vectors are added in group order.
+//   SPLIT = false: one block per (token, head) writes the output.
+//   SPLIT = true (few tokens, i.e. decode): the keys of each (token, head)
+//   are cut into S consecutive chunks, one block each, which write their
+//   partial max, sum and unnormalised output to a workspace;
+//   attention_combine_kernel merges the S chunks in order.
+// Every result depends on the position only, never on timing.
+template <int LPK, bool SPLIT>
 __global__ __launch_bounds__(256) void attention_kernel(const float *qs, const _Float16 *kc,
                                                         const _Float16 *vc, _Float16 *out,
-                                                        int pos0, int heads, int hd) {
-    extern __shared__ float sc[];
+                                                        float *ws, int pos0, int heads, int S) {
+    constexpr int HD = LPK * 8;
+    constexpr int G = 256 / LPK;                    // lane groups (keys per step)
+    extern __shared__ float smem[];                 // scores [chunk], then partials [G][HD]
     __shared__ float red[4];
-    const int t = blockIdx.x / heads, h = blockIdx.x % heads;
-    const int d = heads * hd;
+    const int bh = SPLIT ? blockIdx.x / S : blockIdx.x;
+    const int split = SPLIT ? blockIdx.x % S : 0;
+    const int t = bh / heads, h = bh % heads;
+    const int d = heads * HD;
     const int nk = pos0 + t + 1;
-    const float *q = qs + (long)t * d + h * hd;
-    const float scale = 1.0f / sqrtf((float)hd);
-    for (int j = threadIdx.x; j < nk; j += 256) {
-        const _Float16 *kr = kc + (long)j * d + h * hd;
+    const int chunk = SPLIT ? (pos0 + (int)(gridDim.x / S / heads) + S - 1) / S : nk;   // same for every token
+    const int j0 = split * chunk, j1 = min(nk, j0 + chunk);
+    float *sc = smem;
+    float *part = smem + ((chunk + 3) & ~3);
+    const int grp = threadIdx.x / LPK, l = threadIdx.x % LPK;
+    const float scale = 1.0f / sqrtf((float)HD);
+
+    float q[8];
+    {
+        const float *qp = qs + (long)t * d + h * HD + 8 * l;
+        const f4 q0 = *(const f4 *)qp, q1 = *(const f4 *)(qp + 4);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            q[e] = q0[e];
+            q[4 + e] = q1[e];
+        }
+    }
+    const _Float16 *kb = kc + h * HD + 8 * l;
+    const _Float16 *vb = vc + h * HD + 8 * l;
+    for (int j = j0 + grp; j < j1; j += G) {
+        const h8 k = *(const h8 *)(kb + (long)j * d);
         float s = 0.0f;
-        for (int i = 0; i < hd; ++i) s = fmaf(q[i], (float)kr[i], s);
-        sc[j] = s * scale;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) s = fmaf(q[e], (float)k[e], s);
+#pragma unroll
+        for (int off = LPK / 2; off >= 1; off >>= 1) s += __shfl_xor(s, off);
+        if (l == 0) sc[j - j0] = s * scale;
     }
     __syncthreads();
     float m = -INFINITY;
-    for (int j = threadIdx.x; j < nk; j += 256) m = fmaxf(m, sc[j]);
+    for (int j = j0 + threadIdx.x; j < j1; j += 256) m = fmaxf(m, sc[j - j0]);
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
     if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
@@ -1178,32 +1240,124 @@ __global__ __launch_bounds__(256) void attention_kernel(const float *qs, const _
     m = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
     __syncthreads();
     float sum = 0.0f;
-    for (int j = threadIdx.x; j < nk; j += 256) {
-        float e = expf(sc[j] - m);
-        sc[j] = e;
+    for (int j = j0 + threadIdx.x; j < j1; j += 256) {
+        const float e = expf(sc[j - j0] - m);
+        sc[j - j0] = e;
         sum += e;
     }
-    sum = block_sum_256(sum, red);
+    sum = block_sum_256(sum, red);   // also orders the sc[] writes before the reads below
+    float o[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) o[e] = 0.0f;
+    for (int j = j0 + grp; j < j1; j += G) {
+        const h8 v = *(const h8 *)(vb + (long)j * d);
+        const float p = sc[j - j0];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o[e] = fmaf(p, (float)v[e], o[e]);
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) part[grp * HD + 8 * l + e] = o[e];
+    __syncthreads();
+    if (SPLIT) {
+        // chunk record: [HD] unnormalised output, then max, sum (an empty
+        // chunk has max -inf and sum 0 and adds nothing when merged)
+        float *rec = ws + (long)blockIdx.x * (HD + 2);
+        for (int i = threadIdx.x; i < HD; i += 256) {
+            float acc = 0.0f;
+            for (int g2 = 0; g2 < G; ++g2) acc += part[g2 * HD + i];
+            rec[i] = acc;
+        }
+        if (threadIdx.x == 0) {
+            rec[HD] = j0 < j1 ? m : -INFINITY;
+            rec[HD + 1] = sum;
+        }
+        return;
+    }
     const float inv = 1.0f / sum;
-    for (int i = threadIdx.x; i < hd; i += 256) {
-        float o = 0.0f;
-        for (int j = 0; j < nk; ++j) o = fmaf(sc[j], (float)vc[(long)j * d + h * hd + i], o);
-        out[(long)t * d + h * hd + i] = (_Float16)(o * inv);
+    for (int i = threadIdx.x; i < HD; i += 256) {
+        float acc = 0.0f;
+        for (int g2 = 0; g2 < G; ++g2) acc += part[g2 * HD + i];
+        out[(long)t * d + h * HD + i] = (_Float16)(acc * inv);
     }
 }
 
+// Merges the S chunk records of each (token, head) in chunk order:
+// out = sum_s exp(m_s - M) o_s / sum_s exp(m_s - M) l_s with M = max_s m_s.
+__global__ __launch_bounds__(256) void attention_combine_kernel(const float *ws, _Float16 *out,
+                                                                int heads, int hd, int S) {
+    const int bh = blockIdx.x;
+    const int t = bh / heads, h = bh % heads;
+    const float *rec = ws + (long)bh * S * (hd + 2);
+    float M = -INFINITY;
+    for (int s = 0; s < S; ++s) M = fmaxf(M, rec[s * (hd + 2) + hd]);
+    float L = 0.0f;
+    for (int s = 0; s < S; ++s) {
+        const float ms = rec[s * (hd + 2) + hd];
+        if (ms != -INFINITY) L += expf(ms - M) * rec[s * (hd + 2) + hd + 1];
+    }
+    const float inv = 1.0f / L;
+    for (int i = threadIdx.x; i < hd; i += 256) {
+        float acc = 0.0f;
+        for (int s = 0; s < S; ++s) {
+            const float ms = rec[s * (hd + 2) + hd];
+            if (ms != -INFINITY) acc += expf(ms - M) * rec[s * (hd + 2) + i];
+        }
+        out[(long)t * heads * hd + h * hd + i] = (_Float16)(acc * inv);
+    }
+}
+
+int64_t attention_workspace_floats(int head_dim) { return (int64_t)kAttnWsRecords * (head_dim + 2); }
+
 hipError_t launch_attention(const void *qkv, void *kcache, void *vcache, void *q_scratch,
-                            void *out, int T, int pos0, int heads, int head_dim, float theta,
-                            hipStream_t s) {
-    hipLaunchKernelGGL(rope_append_kernel, dim3(T), dim3(256), 0, s, (const _Float16 *)qkv,
-                       (float *)q_scratch, (_Float16 *)kcache, (_Float16 *)vcache, pos0, heads,
-                       head_dim, theta);
+                            void *out, float *ws, int T, int pos0, int heads, int head_dim,
+                            float theta, hipStream_t s) {
+    if (head_dim % 8 || head_dim < 8 || head_dim > 512 || (head_dim & (head_dim - 1)))
+        return hipErrorInvalidValue;   // power of two, 8 .. 512
+    hipLaunchKernelGGL(rope_append_kernel, dim3(T), dim3(256), (size_t)head_dim * sizeof(float), s,
+                       (const _Float16 *)qkv, (float *)q_scratch, (_Float16 *)kcache,
+                       (_Float16 *)vcache, pos0, heads, head_dim, theta);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    size_t lds = (size_t)(pos0 + T) * sizeof(float);
-    hipLaunchKernelGGL(attention_kernel, dim3(T * heads), dim3(256), lds, s,
-                       (const float *)q_scratch, (const _Float16 *)kcache,
-                       (const _Float16 *)vcache, (_Float16 *)out, pos0, heads, head_dim);
+    const int lpk = head_dim / 8;
+    const int nk_max = pos0 + T;
+    // few (token, head) pairs: split the keys so that about 256 blocks run,
+    // each over at least 64 keys, within the workspace
+    int S = 1;
+    if (ws && T * heads < 256) {
+        S = std::min(std::min(16, (256 + T * heads - 1) / (T * heads)), (nk_max + 63) / 64);
+        while (S > 1 && (int64_t)T * heads * S > kAttnWsRecords) --S;
+    }
+    const int chunk = S > 1 ? (nk_max + S - 1) / S : nk_max;
+    const size_t lds = ((size_t)((chunk + 3) & ~3) + (size_t)(256 / lpk) * head_dim) * sizeof(float);
+    auto go = [&](auto kern) {
+        hipLaunchKernelGGL(kern, dim3(T * heads * S), dim3(256), lds, s, (const float *)q_scratch,
+                           (const _Float16 *)kcache, (const _Float16 *)vcache, (_Float16 *)out, ws,
+                           pos0, heads, S);
+    };
+    if (S > 1) {
+        switch (lpk) {
+        case 1: go(attention_kernel<1, true>); break;
+        case 2: go(attention_kernel<2, true>); break;
+        case 4: go(attention_kernel<4, true>); break;
+        case 8: go(attention_kernel<8, true>); break;
+        case 16: go(attention_kernel<16, true>); break;
+        case 32: go(attention_kernel<32, true>); break;
+        default: go(attention_kernel<64, true>); break;
+        }
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        hipLaunchKernelGGL(attention_combine_kernel, dim3(T * heads), dim3(256), 0, s,
+                           (const float *)ws, (_Float16 *)out, heads, head_dim, S);
+        return hipGetLastError();
+    }
+    switch (lpk) {
+    case 1: go(attention_kernel<1, false>); break;
+    case 2: go(attention_kernel<2, false>); break;
+    case 4: go(attention_kernel<4, false>); break;
+    case 8: go(attention_kernel<8, false>); break;
+    case 16: go(attention_kernel<16, false>); break;
+    case 32: go(attention_kernel<32, false>); break;
+    default: go(attention_kernel<64, false>); break;
+    }
     return hipGetLastError();
 }
 

@@ -230,6 +230,8 @@ int validate_layers(std::vector<Layer> &layers, int from, std::vector<Slot> &slo
         case SN_OP_ATTENTION: {
             if (d.heads <= 0 || d.head_dim <= 0 || d.head_dim % 2 || d.kv_layer < 0 || d.max_seq <= 0)
                 return set_err(err, at + "bad attention geometry"), SN_E_INVALID;
+            if (d.head_dim < 8 || d.head_dim > 512 || (d.head_dim & (d.head_dim - 1)))
+                return set_err(err, at + "head_dim must be a power of two in [8, 512]"), SN_E_UNSUPPORTED;
             int dm = d.heads * d.head_dim;
             if (src->c != 3 * dm || d.c_in != 3 * dm || d.c_out != dm)
                 return set_err(err, at + "attention expects [T][3d] -> [T][d]"), SN_E_INVALID;

@@ -52,7 +52,7 @@ class SnStats(C.Structure):
                 ("activation_bytes", C.c_int64), ("kv_bytes", C.c_int64),
                 ("table_bytes", C.c_int64), ("n_slabs", C.c_int32), ("n_pieces", C.c_int32),
                 ("n_layers", C.c_int32), ("resident", C.c_int32), ("n_infers", C.c_int64),
-                ("last_ms", C.c_double)]
+                ("last_ms", C.c_double), ("input_bytes", C.c_int64), ("output_bytes", C.c_int64)]
 
 
 class SnSlabInfo(C.Structure):
@@ -162,9 +162,22 @@ class SwapNet:
     def plan(self):
         return self._check(self.lib.sn_plan(self.ctx))
 
+    def _host_buffers(self, x, dtype):
+        # the library reads / writes exactly input_bytes / output_bytes
+        st = self.stats()
+        if x is not None and x.nbytes != st["input_bytes"]:
+            raise ValueError("input has %d bytes, the network takes %d" % (x.nbytes, st["input_bytes"]))
+        shape = self.out_shape if self.out_shape is not None else \
+            (st["output_bytes"] // np.dtype(dtype).itemsize,)
+        out = np.empty(shape, dtype)
+        if out.nbytes != st["output_bytes"]:
+            raise ValueError("output shape %s holds %d bytes, the network writes %d"
+                             % (shape, out.nbytes, st["output_bytes"]))
+        return out
+
     def infer(self, x):
         x = np.ascontiguousarray(x, np.float16)
-        out = np.empty(self.out_shape, self.out_dtype)
+        out = self._host_buffers(x, self.out_dtype)
         self._check(self.lib.sn_infer(self.ctx, x.ctypes.data_as(C.c_void_p),
                                       out.ctypes.data_as(C.c_void_p)))
         return out
@@ -176,7 +189,7 @@ class SwapNet:
 
     def infer_tokens(self, ids):
         ids = np.ascontiguousarray(ids, np.int32)
-        out = np.empty(self.out_shape, np.float32)
+        out = self._host_buffers(None, np.float32)
         self._check(self.lib.sn_infer_tokens(self.ctx, ids.ctypes.data_as(C.c_void_p), len(ids),
                                              out.ctypes.data_as(C.c_void_p)))
         return out

@@ -215,6 +215,26 @@ def test_decoder_teacher_forced_parity():
             assert np.array_equal(first.view(np.uint32), got.view(np.uint32))
 
 
+def test_decoder_long_context_split_attention():
+    # 200-token prompt: single-token steps attend over 200+ cached positions,
+    # which the attention kernel splits over several blocks (per-chunk
+    # partials merged in order); teacher-forced against the oracle
+    net = small_decoder(max_seq=224, prompt=200, gen=6)
+    wts = W.make_weights(net)
+    prompt = W.make_input(net)
+    gen = net.extra["gen"]
+    with S.build_engine(net, wts, budget=1 << 30) as eng:
+        rows, fed = [eng.infer_tokens(prompt)], []
+        for _ in range(gen - 1):
+            nxt = int(np.argmax(rows[-1]))
+            fed.append(nxt)
+            rows.append(eng.infer_tokens(np.array([nxt], np.int32)))
+    seq = np.concatenate([prompt, np.array(fed, np.int32)])
+    want = oracle.decoder_forward(net, wts, seq)[len(prompt) - 1:]
+    for t in range(gen):
+        assert rel_err(rows[t], want[t]) <= TOL, t
+
+
 def test_decoder_prefill_uses_mfma_path_and_decode_matches_prefix():
     """Logits of a prompt processed in one call equal (to the bar) the logits
     of the same tokens fed one by one (GEMM path vs GEMV path)."""

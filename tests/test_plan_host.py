@@ -35,7 +35,7 @@ def test_library_exports_every_declared_symbol():
 def test_struct_sizes_match_header_layout():
     # sn_layer: 19 int32 + 2 float + 4 int64 = 76 + 8 + 32 -> 120 with alignment
     assert C.sizeof(S.SnLayer) == 120
-    assert C.sizeof(S.SnStats) == 7 * 8 + 4 * 4 + 8 + 8
+    assert C.sizeof(S.SnStats) == 7 * 8 + 4 * 4 + 8 + 8 + 2 * 8
 
 
 def plan_of(name, budget=None, **kw):
@@ -266,3 +266,27 @@ def test_token_network_errors():
     lg = np.zeros(10, np.float32)
     assert lib.sn_infer_tokens(eng.ctx, ids.ctypes.data_as(C.c_void_p), 4,
                                lg.ctypes.data_as(C.c_void_p)) in (S.SN_E_UNSUPPORTED,)
+
+
+def test_host_buffers_sized_from_the_library():
+    # sn_stats reports the bytes sn_infer reads and writes; the binding sizes
+    # its buffers from them and refuses mismatched inputs before any call
+    net = W.tiny_cnn()
+    eng = S.build_engine(net, lambda li: W.layer_params(net, li), host_only=True)
+    st = eng.stats()
+    assert st["input_bytes"] == 3 * 32 * 32 * 2
+    assert st["output_bytes"] == 10 * 2
+    with pytest.raises(ValueError):
+        eng.infer(np.zeros((3, 16, 16), np.float16))
+    eng.out_shape = (3,)
+    with pytest.raises(ValueError):
+        eng.infer(np.zeros((3, 32, 32), np.float16))
+    eng.out_shape = None   # unknown shape: a flat buffer of output_bytes
+    with pytest.raises(S.SwapNetError):   # host-only contexts cannot run
+        eng.infer(np.zeros((3, 32, 32), np.float16))
+    eng.close()
+    dec = W.decoder7b(n_layers=1, d=64, heads=2, ffn=96, vocab=100, max_seq=16, prompt=4, gen=2)
+    eng = S.build_engine(dec, lambda li: W.layer_params(dec, li), host_only=True)
+    st = eng.stats()
+    assert st["input_bytes"] == 0 and st["output_bytes"] == 100 * 4
+    eng.close()
