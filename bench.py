@@ -50,6 +50,12 @@ def parse():
     ap.add_argument("--no-graph", action="store_true", help="enqueue call by call (no HIP graph)")
     ap.add_argument("--swapin", type=int, default=2, choices=[0, 1, 2],
                     help="0 copy kernel, 1 SDMA from the calling thread, 2 SDMA from the copy thread")
+    ap.add_argument("--partition", type=int, default=0, choices=[0, 1],
+                    help="0: slabs follow the workload's blocks; 1: balanced re-cut into "
+                         "ceil(2 s / B) equal slabs")
+    ap.add_argument("--sync", type=int, default=0, choices=[0, 1],
+                    help="copy thread ordering: 0 events + signal kernels, "
+                         "1 stream write/wait of values in mapped memory")
     ap.add_argument("--copy-streams", type=int, default=1, choices=[1, 2],
                     help="DMA queues used by the copy thread (consecutive slabs alternate)")
     ap.add_argument("--swapin-blocks", type=int, default=None,
@@ -309,6 +315,7 @@ def bench_decoder(a, torch, S, W):
     budget = net.budget_bytes()
     log("building swapped decoder (budget %d B = 4 layers)" % budget)
     eng = build_decoder(S, W, net, budget)
+    eng.set_option(S.OPT_SYNC, a.sync)
     st = eng.stats()
     log("timing prefill + %d decode steps (swapped)" % (gen - 1))
     run_decoder(eng, prompt[:8], 3)                      # warm-up
@@ -376,11 +383,12 @@ def main():
                 "tiny_cnn": "0.6"}[net.name] if a.budget_frac is None else "%.4f" % a.budget_frac
 
     log("planning swapped engine (budget %d B) and resident engine" % budget)
-    eng_sw = S.build_engine(net, wts, budget=budget)
+    eng_sw = S.build_engine(net, wts, budget=budget, partition=a.partition)
     st = eng_sw.stats()
     eng_res = S.build_engine(net, wts, budget=st["image_bytes"] + 4096)
     eng_sw.set_option(S.OPT_SWAPIN, a.swapin)
     eng_sw.set_option(S.OPT_COPY_STREAMS, a.copy_streams)
+    eng_sw.set_option(S.OPT_SYNC, a.sync)
     if a.swapin_blocks:
         eng_sw.set_option(S.OPT_SWAPIN_BLOCKS, a.swapin_blocks)
     if a.no_graph:
@@ -458,7 +466,10 @@ def main():
         "config": {"workload": net.name, "batch": 1, "input": "x".join(map(str, net.input_shape)),
                    "weight_bytes": net.weight_bytes(), "budget_bytes": budget,
                    "budget_fraction": frac_txt, "user_blocks": len(net.blocks),
-                   "slabs": st["n_slabs"], "parallelism": "none (1 GPU)"},
+                   "slabs": st["n_slabs"],
+                   "partition": "balanced" if a.partition else "workload blocks",
+                   "sync": ["events", "stream values"][a.sync],
+                   "parallelism": "none (1 GPU)"},
         "swapped_ms": round(sw_ms, 4), "resident_ms": round(res_ms, 4),
         "swapped_latency_ms": round(sw_lat, 4), "resident_latency_ms": round(res_lat, 4),
         "swapped_wall_ms": round(sw_wall, 4), "resident_wall_ms": round(res_wall, 4),

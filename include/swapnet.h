@@ -178,6 +178,24 @@ enum sn_option {
                                    that one queue's per-copy start-up overlaps
                                    the other's transfer (the two then share
                                    the link, which delays each slab)          */
+    SN_OPT_PARTITION = 8,       /* 0 (default): slabs follow the user blocks,
+                                   split only where the pair constraint
+                                   (Eq. 3) requires; 1: the layers of all
+                                   blocks are re-cut into n = ceil(2 s / B)
+                                   slabs of about s / n bytes each (Sec. 6:
+                                   m = 2 parallel blocks of equal share),
+                                   cutting layers by output channels where a
+                                   slab boundary falls inside one; fewer,
+                                   larger DMAs at small budgets               */
+    SN_OPT_SYNC = 9,            /* copy-thread mode (SN_OPT_SWAPIN 2): how
+                                   the copy and compute streams order each
+                                   other.  0: hipEvents for "slab loaded" and
+                                   a one-thread kernel that bumps a mapped
+                                   counter for "slab computed"; 1: stream
+                                   writes / waits of 64-bit values in mapped
+                                   memory (hipStreamWriteValue64 /
+                                   hipStreamWaitValue64) for both.  May be
+                                   set after plan, between inferences         */
     SN_OPT_GRAPH = 4            /* 1 (default): the kernels of each slab of an
                                    image network are captured once per
                                    (input, output) buffer pair into one HIP

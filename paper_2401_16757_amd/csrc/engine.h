@@ -76,7 +76,7 @@ int validate_layers(std::vector<Layer> &layers, int from, std::vector<Slot> &slo
                     std::string &err);
 int prepack_layer(Layer &L, const uint8_t *blob, size_t blob_bytes, std::string &err);
 int plan_slabs(const std::vector<Layer> &layers, int n_blocks, int64_t split_budget,
-               int64_t max_slab, PlanResult &out, std::string &err);
+               int64_t max_slab, bool balanced, PlanResult &out, std::string &err);
 int place_slabs(PlanResult &p, int64_t arena_budget, std::string &err);
 void assign_slot_offsets(std::vector<Slot> &slots, int64_t &total);
 void write_image(const std::vector<Layer> &layers, const PlanResult &p, uint8_t *image);

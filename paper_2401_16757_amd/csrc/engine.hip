@@ -83,11 +83,15 @@ struct sn_ctx {
     // completion counters written by the compute stream (signal kernels) in
     // pinned host memory: [0, ns) per slab, ns = inference start
     unsigned long long *sig_host = nullptr, *sig_dev = nullptr;
+    // per-slab "swap-in done" values written by the copy stream (SN_OPT_SYNC 1)
+    unsigned long long *lflag_host = nullptr, *lflag_dev = nullptr;
+    int sync = 0;                      // SN_OPT_SYNC
     std::atomic<int> copy_error{0};
     std::string copy_err;
     uint8_t *act = nullptr;
     int64_t act_bytes = 0;
     uint8_t *kv = nullptr;
+    int partition = 0;                 // SN_OPT_PARTITION
     int64_t kv_bytes = 0;
     int64_t attn_ws_bytes = 0;
     int kv_layers = 0, max_seq = 0, d_model = 0, max_tokens = 0;
@@ -247,6 +251,17 @@ extern "C" int sn_set_option(sn_ctx *c, int option, int64_t value) {
         if (value < 0) return fail(c, SN_E_INVALID, "negative max slab");
         c->max_slab = value;
         return SN_OK;
+    case SN_OPT_SYNC:
+        if (value != 0 && value != 1) return fail(c, SN_E_INVALID, "sync must be 0 or 1");
+        if (c->state == ST_PLANNED && c->have_prev) wait_copier_idle(c);
+        if ((int)value != c->sync) drop_graphs(c);   // the graphs hold the signal kernels
+        c->sync = (int)value;
+        return SN_OK;
+    case SN_OPT_PARTITION:
+        if (c->state != ST_ADDING) return fail(c, SN_E_STATE, "partition is fixed at plan");
+        if (value != 0 && value != 1) return fail(c, SN_E_INVALID, "partition must be 0 or 1");
+        c->partition = (int)value;
+        return SN_OK;
     default:
         return fail(c, SN_E_INVALID, "unknown option");
     }
@@ -275,7 +290,8 @@ extern "C" int sn_plan(sn_ctx *c) {
     const int L = (int)c->layers.size();
     // the network output stays live to the end
     c->slots[c->layers[L - 1].d.dst].last = L;
-    int rc = plan_slabs(c->layers, c->n_blocks, c->split_budget, c->max_slab, c->plan, err);
+    int rc = plan_slabs(c->layers, c->n_blocks, c->split_budget, c->max_slab, c->partition == 1,
+                        c->plan, err);
     if (rc) return fail(c, rc, err);
     rc = place_slabs(c->plan, c->budget, err);
     if (rc) return fail(c, rc, err);
@@ -404,6 +420,10 @@ extern "C" int sn_plan(sn_ctx *c) {
                                  hipHostMallocMapped));
         memset(c->sig_host, 0, (ns + 1) * sizeof(unsigned long long));
         HIP_TRY(c, hipHostGetDevicePointer((void **)&c->sig_dev, c->sig_host, 0));
+        HIP_TRY(c, hipHostMalloc((void **)&c->lflag_host, ns * sizeof(unsigned long long),
+                                 hipHostMallocMapped));
+        memset(c->lflag_host, 0, ns * sizeof(unsigned long long));
+        HIP_TRY(c, hipHostGetDevicePointer((void **)&c->lflag_dev, c->lflag_host, 0));
         start_copier(c);
     }
     if (c->plan.resident) {
@@ -607,7 +627,9 @@ static void copier_main(sn_ctx *c) {
                 e = hipMemcpyAsync(c->arena + s.arena_off, c->image + s.image_off, (size_t)s.bytes,
                                    hipMemcpyHostToDevice, q);
             if (e == hipSuccess && c->timing) e = hipEventRecord(c->t_in1[i], q);
-            if (e == hipSuccess) e = hipEventRecord(c->loaded[i], q);
+            if (e == hipSuccess)
+                e = c->sync == 1 ? hipStreamWriteValue64(q, c->lflag_dev + i, seq, 0)
+                                 : hipEventRecord(c->loaded[i], q);
             if (e != hipSuccess && !c->copy_error.load()) {
                 c->copy_err = std::string("swap-in DMA: ") + hipGetErrorString(e);
                 c->copy_error.store(1);
@@ -623,6 +645,14 @@ static void copier_main(sn_ctx *c) {
 static void wait_copier_idle(sn_ctx *c) {
     if (!c->copier.joinable()) return;
     while (c->handled.load() < c->tseq) cpu_relax();
+}
+
+// After a synchronous inference: a swap-in the copy thread failed to issue.
+static int check_copier(sn_ctx *c) {
+    if (!c->copier.joinable()) return SN_OK;
+    wait_copier_idle(c);
+    if (c->copy_error.exchange(0)) return fail(c, SN_E_HIP, c->copy_err);
+    return SN_OK;
 }
 
 static void start_copier(sn_ctx *c) {
@@ -684,6 +714,15 @@ static int slab_kernels(sn_ctx *c, int i, int n_tok, hipStream_t cs) {
 // `pre` / `post` run on `cs` around the first / last slab's kernels (input
 // and output conversion).  With `graphs`, slab i's kernels (with pre / post
 // for the first / last slab) are replayed from graphs[i] instead.
+// Marks, on the compute stream, that slab i's compute of inference `seq`
+// (i == number of slabs: the start of the inference) has completed, for the
+// copy thread polling sig_host[i]: the counter reaches `seq`.  SN_OPT_SYNC 0:
+// a one-thread kernel increments it; 1: a stream write of the value.
+static hipError_t signal_done(sn_ctx *c, int i, uint64_t seq, hipStream_t cs) {
+    if (c->sync == 1) return hipStreamWriteValue64(cs, c->sig_dev + i, seq, 0);
+    return launch_signal(c->sig_dev + i, cs);
+}
+
 template <typename Pre, typename Post>
 static int run_slabs(sn_ctx *c, int n_tok, hipStream_t cs, Pre pre, Post post, bool graphs) {
     const int ns = (int)c->plan.slabs.size();
@@ -722,7 +761,7 @@ static int run_slabs(sn_ctx *c, int n_tok, hipStream_t cs, Pre pre, Post post, b
         return SN_OK;
     };
     if (threaded) {
-        hipError_t e = launch_signal(c->sig_dev + ns, cs);
+        hipError_t e = signal_done(c, ns, seq, cs);
         if (e != hipSuccess) return abort_copies(fail(c, SN_E_HIP, std::string("signal: ") + hipGetErrorString(e)));
         c->fork_seq.store(seq, std::memory_order_release);
         {
@@ -734,22 +773,33 @@ static int run_slabs(sn_ctx *c, int n_tok, hipStream_t cs, Pre pre, Post post, b
         return rc;
     }
     for (int i = 0; i < ns; ++i) {
+        // the compute stream may only wait for slab i once the copy thread
+        // has enqueued what ends that wait (loaded[i], or the write of the
+        // flag): HIP streams beyond the hardware-queue count share in-order
+        // hardware queues, where a wait enqueued ahead of its producer would
+        // block that producer for good
         if (threaded) {
             while (c->loaded_seq[i].load(std::memory_order_acquire) < seq) cpu_relax();
             if (c->copy_error.load()) return abort_copies(fail(c, SN_E_HIP, c->copy_err));
         }
         hipError_t e = hipSuccess;
-        if (swap) e = hipStreamWaitEvent(cs, c->loaded[i], 0);
+        if (threaded && c->sync == 1)
+            e = hipStreamWaitValue64(cs, c->lflag_dev + i, seq, hipStreamWaitValueGte);
+        else if (swap)
+            e = hipStreamWaitEvent(cs, c->loaded[i], 0);
         if (e == hipSuccess && c->timing) e = hipEventRecord(c->t_ex0[i], cs);
         if (e != hipSuccess) return abort_copies(fail(c, SN_E_HIP, hipGetErrorString(e)));
         if (graphs) {
             if ((e = hipGraphLaunch(c->graphs[i], cs)) != hipSuccess)
                 return abort_copies(fail(c, SN_E_HIP, std::string("graph launch: ") + hipGetErrorString(e)));
+            // (with SN_OPT_SYNC 0 the graph ends with the signal kernel)
+            if (threaded && c->sync == 1 && (e = signal_done(c, i, seq, cs)) != hipSuccess)
+                return abort_copies(fail(c, SN_E_HIP, std::string("signal: ") + hipGetErrorString(e)));
         } else {
             if (i == 0 && (rc = pre(cs))) return abort_copies(rc);
             if ((rc = slab_kernels(c, i, n_tok, cs))) return abort_copies(rc);
             if (i == ns - 1 && (rc = post(cs))) return abort_copies(rc);
-            if (threaded && (e = launch_signal(c->sig_dev + i, cs)) != hipSuccess)
+            if (threaded && (e = signal_done(c, i, seq, cs)) != hipSuccess)
                 return abort_copies(fail(c, SN_E_HIP, std::string("signal: ") + hipGetErrorString(e)));
         }
         if (c->timing) e = hipEventRecord(c->t_ex1[i], cs);
@@ -848,7 +898,7 @@ static int capture_graphs(sn_ctx *c, const void *d_in, void *d_out) {
         if (i == 0) rc = convert_input(c, d_in, c->comp_s);
         if (!rc) rc = slab_kernels(c, i, 1, c->comp_s);
         if (!rc && i == ns - 1) rc = convert_output(c, d_out, c->comp_s);
-        if (!rc && !c->plan.resident && c->swapin == 2) {
+        if (!rc && !c->plan.resident && c->swapin == 2 && c->sync == 0) {
             hipError_t e = launch_signal(c->sig_dev + i, c->comp_s);
             if (e != hipSuccess) rc = fail(c, SN_E_HIP, std::string("signal: ") + hipGetErrorString(e));
         }
@@ -914,6 +964,7 @@ extern "C" int sn_infer(sn_ctx *c, const void *input, void *output) {
     }
     HIP_TRY(c, hipMemcpyAsync(output, c->out_stage, (size_t)c->out_bytes, hipMemcpyDeviceToHost, c->comp_s));
     HIP_TRY(c, hipStreamSynchronize(c->comp_s));
+    if ((rc = check_copier(c))) return rc;
     collect_timing(c);
     c->last_ms = std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();
     return SN_OK;
@@ -947,6 +998,7 @@ extern "C" int sn_infer_tokens(sn_ctx *c, const int32_t *ids, int n_ids, float *
     HIP_TRY(c, hipEventRecord(c->ev_end, cs));
     c->have_prev = true;
     HIP_TRY(c, hipStreamSynchronize(cs));
+    if ((rc = check_copier(c))) return rc;
     collect_timing(c);
     c->pos += n_ids;
     c->n_infers++;
@@ -1061,6 +1113,7 @@ extern "C" void sn_destroy(sn_ctx *c) {
         if (c->image) hipHostFree(c->image);
         if (c->table_host) hipHostFree(c->table_host);
         if (c->sig_host) hipHostFree(c->sig_host);
+        if (c->lflag_host) hipHostFree(c->lflag_host);
         for (void *p : {(void *)c->arena, (void *)c->act, (void *)c->kv, (void *)c->d_ids,
                         (void *)c->q_scratch, (void *)c->attn_ws, c->in_stage, c->out_stage,
                         (void *)c->ws})

@@ -393,14 +393,120 @@ bool split_slab(const std::vector<Layer> &layers, const SlabSpec &s, int64_t tar
 }
 }  // namespace
 
+// Balanced partition (Sec. 6: m = 2 blocks in flight, n = ceil(m s / b),
+// rounded up to even): the layers of all blocks, in order, are cut into
+// slabs of at most ceil(s / n) bytes (never more than half the budget, so any two consecutive
+// slabs fit side by side); a layer that straddles a boundary is cut by
+// output units, the part that fits closing the current slab.
+static int balanced_slabs(const std::vector<Layer> &layers, int64_t B, int64_t max_slab,
+                          std::vector<SlabSpec> &slabs, std::string &err) {
+    int64_t total = 0;
+    for (int li = 0; li < (int)layers.size(); ++li)
+        total += piece_bytes(layers, PS{li, 0, layers[li].units ? layers[li].units : 0});
+    int64_t cap = B / 2 / kAlign * kAlign;
+    if (max_slab > 0) cap = std::min(cap, max_slab);
+    if (cap <= 0) {
+        err = "infeasible: budget too small to partition";
+        return SN_E_INFEASIBLE;
+    }
+    // n even: slabs alternate between the two ends of the arena, so with an
+    // even count the last slab sits at the other end from slab 0 and the next
+    // inference's first swap-in overlaps the last slab's compute
+    int64_t n = std::max<int64_t>(1, (2 * total + B - 1) / std::max<int64_t>(B, 1));
+    if (n > 1 && (n & 1)) ++n;
+    const int64_t target = std::min(cap, (total + n - 1) / n);
+    slabs.clear();
+    SlabSpec cur;
+    int64_t acc = 0;
+    auto close = [&]() {
+        if (!cur.empty()) slabs.push_back(cur);
+        cur.clear();
+        acc = 0;
+    };
+    for (int li = 0; li < (int)layers.size(); ++li) {
+        const Layer &L = layers[li];
+        int64_t u0 = 0;
+        const int64_t u1 = L.units ? L.units : 0;
+        for (;;) {
+            const int64_t b = piece_bytes(layers, PS{li, u0, u1});
+            if (acc + b <= target || b == 0) {
+                cur.push_back(PS{li, u0, u1});
+                acc += b;
+                break;
+            }
+            // the largest number of units that still fits the current slab
+            int64_t lo = 0, hi = u1 - u0;
+            const bool splittable = L.units && L.d.op != SN_OP_EMBED && hi >= 2;
+            if (splittable) {
+                while (lo < hi) {
+                    const int64_t mid = (lo + hi + 1) / 2;
+                    if (acc + piece_bytes(layers, PS{li, u0, u0 + mid}) <= target) lo = mid;
+                    else hi = mid - 1;
+                }
+            }
+            if (lo > 0) {
+                cur.push_back(PS{li, u0, u0 + lo});
+                u0 += lo;
+                close();
+                continue;
+            }
+            if (!cur.empty()) {
+                close();
+                continue;
+            }
+            // an empty slab cannot take it: one unit is larger than the target
+            if (b > cap && !splittable) {
+                err = "infeasible: layer " + std::to_string(li) + " (" + std::to_string(b) +
+                      " bytes) exceeds half the budget and cannot be split";
+                return SN_E_INFEASIBLE;
+            }
+            const int64_t one = piece_bytes(layers, PS{li, u0, u0 + 1});
+            if (one > cap) {
+                err = "infeasible: one output unit of layer " + std::to_string(li) +
+                      " exceeds half the budget";
+                return SN_E_INFEASIBLE;
+            }
+            // fill up to the cap instead of the target
+            int64_t k = 1;
+            while (u0 + k < u1 && piece_bytes(layers, PS{li, u0, u0 + k + 1}) <= cap) ++k;
+            cur.push_back(PS{li, u0, u0 + k});
+            u0 += k;
+            close();
+            if (u0 >= u1) break;
+        }
+    }
+    close();
+    // alignment padding can leave a small remainder slab: fold it into the
+    // previous one when that stays within half the budget
+    if (slabs.size() >= 2) {
+        const int64_t last = slab_bytes(layers, slabs.back());
+        const int64_t prev = slab_bytes(layers, slabs[slabs.size() - 2]);
+        if (4 * last < target && prev + last <= cap) {
+            SlabSpec &p = slabs[slabs.size() - 2];
+            p.insert(p.end(), slabs.back().begin(), slabs.back().end());
+            slabs.pop_back();
+        }
+    }
+    return SN_OK;
+}
+
 int plan_slabs(const std::vector<Layer> &layers, int n_blocks, int64_t split_budget,
-               int64_t max_slab, PlanResult &res, std::string &err) {
+               int64_t max_slab, bool balanced, PlanResult &res, std::string &err) {
     const int64_t B = split_budget / kAlign * kAlign;
     std::vector<SlabSpec> slabs(n_blocks);
     for (int li = 0; li < (int)layers.size(); ++li) {
         const Layer &L = layers[li];
         int64_t u1 = L.units ? L.units : 0;
         slabs[L.block].push_back(PS{li, 0, u1});
+    }
+    if (balanced) {
+        int64_t total = 0;
+        for (const SlabSpec &ss : slabs) total += slab_bytes(layers, ss);
+        // a model that fits stays as the user gave it (the run is resident)
+        if (total > B) {
+            int rc = balanced_slabs(layers, B, max_slab, slabs, err);
+            if (rc) return rc;
+        }
     }
     for (int iter = 0; iter < 1000000; ++iter) {
         const int n = (int)slabs.size();

@@ -28,6 +28,8 @@ FLAG_RELU, FLAG_FLATTEN_CHW, FLAG_SWIGLU, FLAG_OUT_F32, FLAG_LAST_ROW = 1, 2, 4,
 CREATE_HOST_ONLY = 1
 OPT_SPLIT_BUDGET, OPT_TIMING, OPT_MAX_SLAB, OPT_GRAPH, OPT_SWAPIN, OPT_SWAPIN_BLOCKS = 1, 2, 3, 4, 5, 6
 OPT_COPY_STREAMS = 7
+OPT_PARTITION = 8
+OPT_SYNC = 9
 
 EXPORTS = ["sn_create", "sn_create_ex", "sn_add_block", "sn_plan", "sn_set_option", "sn_infer",
            "sn_infer_dev", "sn_infer_tokens", "sn_reset", "sn_get_stats", "sn_get_slab",
@@ -308,7 +310,7 @@ def output_shape(net):
 
 
 def build_engine(net, weights, budget=None, blocks=None, split_budget=None, host_only=False,
-                 timing=False, max_slab=0):
+                 timing=False, max_slab=0, partition=0):
     """Create, register and plan an engine for ``net``.  ``weights`` is a list
     of per-layer parameter dicts or a callable li -> dict."""
     eng = SwapNet(budget if budget is not None else net.budget_bytes(), host_only=host_only)
@@ -316,6 +318,8 @@ def build_engine(net, weights, budget=None, blocks=None, split_budget=None, host
         eng.set_option(OPT_SPLIT_BUDGET, split_budget)
     if max_slab:
         eng.set_option(OPT_MAX_SLAB, max_slab)
+    if partition:
+        eng.set_option(OPT_PARTITION, partition)
     if timing:
         eng.set_option(OPT_TIMING, int(timing))
     for a, b in (blocks or net.blocks):

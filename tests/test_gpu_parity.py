@@ -152,13 +152,35 @@ def test_infer_dev_on_torch_stream_matches_host_path():
         assert np.array_equal(yd.cpu().numpy().view(np.uint16), y_host.view(np.uint16))
 
 
-@pytest.mark.parametrize("modes", [(2,), (1,), (0,), (2, 1, 0, 2)])
+@pytest.mark.parametrize("name,kw,frac", [("resnet50", {"res": 96}, 1 / 5.81),
+                                          ("fcn_resnet101", {"res": 128}, 1 / 3),
+                                          ("vgg16", {"res": 64}, 1 / 4)])
+def test_balanced_partition_matches_resident(name, kw, frac):
+    # the balanced partition (layers re-cut into equal slabs, layers split by
+    # output channels at slab boundaries) computes the same bits as the
+    # all-resident run and matches the oracle
+    net, wts, x, ref = net_case(name, **kw)
+    budget = int(net.weight_bytes() * frac)
+    with S.build_engine(net, wts, budget=budget, partition=1) as eng:
+        assert not eng.stats()["resident"]
+        y = eng.infer(x)
+        y2 = eng.infer(x)
+    with S.build_engine(net, wts, budget=1 << 33) as res:
+        yr = res.infer(x)
+    assert np.array_equal(y.view(np.uint16), yr.view(np.uint16))
+    assert np.array_equal(y2.view(np.uint16), yr.view(np.uint16))
+    assert rel_err(y, ref) <= TOL
+
+
+@pytest.mark.parametrize("modes", [((2, 0),), ((2, 1),), ((1, 0),), ((0, 0),),
+                                   ((2, 1), (1, 0), (2, 0), (0, 0), (2, 1))])
 def test_back_to_back_inferences_with_cross_inference_prefetch(modes):
     # Several inferences queued without a host synchronisation: the next
     # inference's swap-ins of slabs that no earlier slab shares start while
     # the previous one still computes (waiting only for its `wrap` slabs).
     # Every output must equal a one-at-a-time inference of the same input,
-    # bit for bit, in every swap-in mode and when the modes alternate.
+    # bit for bit, in every swap-in mode (the copy thread with either kind of
+    # stream ordering, SN_OPT_SYNC 0 and 1) and when the modes alternate.
     net, wts, x0, _ = net_case("resnet50", res=96)
     rng = np.random.default_rng(7)
     xs = [x0] + [rng.standard_normal(x0.shape).astype(np.float16) for _ in range(3)]
@@ -168,8 +190,9 @@ def test_back_to_back_inferences_with_cross_inference_prefetch(modes):
         want = [eng.infer(x) for x in xs]
         xd = [torch.from_numpy(x).cuda() for x in xs]
         s = torch.cuda.Stream()
-        for mode in modes:
+        for mode, sync in modes:
             eng.set_option(S.OPT_SWAPIN, mode)
+            eng.set_option(S.OPT_SYNC, sync)
             yd = [torch.empty(eng.out_shape, dtype=torch.float16, device="cuda") for _ in xs]
             with torch.cuda.stream(s):
                 for rep in range(2):
@@ -192,8 +215,9 @@ def test_decoder_teacher_forced_parity():
     prompt = W.make_input(net)
     gen = net.extra["gen"]
     lb = sum(l.weight_bytes() for l in net.layers[1:8])
-    for budget, split in ((2 * lb, None), (1 << 30, 2 * lb)):
+    for budget, split, sync in ((2 * lb, None, 0), (2 * lb, None, 1), (1 << 30, 2 * lb, 0)):
         eng = S.build_engine(net, wts, budget=budget, split_budget=split)
+        eng.set_option(S.OPT_SYNC, sync)
         rows, fed = [], []
         logits = eng.infer_tokens(prompt)
         rows.append(logits)
@@ -209,7 +233,7 @@ def test_decoder_teacher_forced_parity():
         want = ref[len(prompt) - 1:]
         for t in range(gen):
             assert rel_err(got[t], want[t]) <= TOL, t
-        if split is None:
+        if split is None and sync == 0:
             first = got
         else:
             assert np.array_equal(first.view(np.uint32), got.view(np.uint32))

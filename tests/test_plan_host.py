@@ -105,18 +105,29 @@ def check_plan(net, eng, budget):
 @pytest.mark.parametrize("name,kw", [("tiny_cnn", {}), ("resnet50", {}), ("vgg16", {}),
                                      ("fcn_resnet101", {})])
 @pytest.mark.parametrize("frac", [None, 1 / 2.32, 1 / 3, 1 / 4, 1 / 5.81])
-def test_plan_invariants(name, kw, frac):
+@pytest.mark.parametrize("partition", [0, 1])
+def test_plan_invariants(name, kw, frac, partition):
     net = W.get_network(name, **kw)
     budget = net.budget_bytes() if frac is None else int(net.weight_bytes() * frac)
     wts = W.make_weights(net)
     try:
-        eng = S.build_engine(net, wts, budget=budget, host_only=True)
+        eng = S.build_engine(net, wts, budget=budget, host_only=True, partition=partition)
     except S.SwapNetError as e:
         # only the tiny network is too small to meet 1/5.81 with 256-byte slabs
         assert e.code == S.SN_E_INFEASIBLE and name == "tiny_cnn", e
         return
     check_plan(net, eng, budget)
     assert eng.stats()["resident"] == 0
+    if partition == 1 and name != "tiny_cnn":
+        # Sec. 6 with m = 2: n = ceil(2 s / B) slabs (rounded up to even) of
+        # near-equal size, each at most half the budget
+        sl = eng.slabs()
+        total = sum(s["bytes"] for s in sl)
+        n = -(-2 * total // (budget // 256 * 256))
+        n += n % 2
+        assert len(sl) in (n - 1, n, n + 1), (len(sl), n)
+        assert max(s["bytes"] for s in sl) <= budget // 2
+        assert max(s["bytes"] for s in sl[:-1]) - min(s["bytes"] for s in sl[:-1]) <= 0.02 * total / len(sl) + 4096
 
 
 def test_slab_counts_of_the_workloads():
