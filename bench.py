@@ -50,9 +50,10 @@ def parse():
     ap.add_argument("--no-graph", action="store_true", help="enqueue call by call (no HIP graph)")
     ap.add_argument("--swapin", type=int, default=2, choices=[0, 1, 2],
                     help="0 copy kernel, 1 SDMA from the calling thread, 2 SDMA from the copy thread")
-    ap.add_argument("--partition", type=int, default=0, choices=[0, 1],
+    ap.add_argument("--partition", type=int, default=0, choices=[0, 1, 2],
                     help="0: slabs follow the workload's blocks; 1: balanced re-cut into "
-                         "ceil(2 s / B) equal slabs")
+                         "ceil(2 s / B) equal slabs; 2: searched under a delay model "
+                         "calibrated on this GPU (on the workload-block plan, untimed)")
     ap.add_argument("--sync", type=int, default=0, choices=[0, 1],
                     help="copy thread ordering: 0 events + signal kernels, "
                          "1 stream write/wait of values in mapped memory")
@@ -382,8 +383,14 @@ def main():
     frac_txt = {"resnet50": "1/2.32", "vgg16": "1/5.81", "fcn_resnet101": "1/3",
                 "tiny_cnn": "0.6"}[net.name] if a.budget_frac is None else "%.4f" % a.budget_frac
 
+    cm = None
+    if a.partition == 2:
+        log("calibrating the delay model on the workload-block plan")
+        with S.build_engine(net, wts, budget=budget) as cal:
+            cal.calibrate(5)
+            cm = cal.cost_model()
     log("planning swapped engine (budget %d B) and resident engine" % budget)
-    eng_sw = S.build_engine(net, wts, budget=budget, partition=a.partition)
+    eng_sw = S.build_engine(net, wts, budget=budget, partition=a.partition, cost_model=cm)
     st = eng_sw.stats()
     eng_res = S.build_engine(net, wts, budget=st["image_bytes"] + 4096)
     eng_sw.set_option(S.OPT_SWAPIN, a.swapin)
@@ -428,6 +435,11 @@ def main():
     chain_ms = measure_copy_chain(torch, [sl["bytes"] for sl in eng_sw.slabs()])
     log("timeline and kernel profile (untimed passes)")
     tl = slab_timeline(S, eng_sw, x)
+    if cm is None:
+        # the delay model of this plan, measured on it (for the prediction)
+        eng_sw.calibrate(5)
+    model = eng_sw.cost_model()
+    pred_lat, pred_per = eng_sw.predict()
     groups = kernel_profile(S, net, eng_res, torch, xd, yr)
     conv = {k: v for k, v in groups.items() if k.startswith("conv")}
     dom = max(conv.items(), key=lambda kv: kv[1][1]) if conv else None
@@ -467,7 +479,7 @@ def main():
                    "weight_bytes": net.weight_bytes(), "budget_bytes": budget,
                    "budget_fraction": frac_txt, "user_blocks": len(net.blocks),
                    "slabs": st["n_slabs"],
-                   "partition": "balanced" if a.partition else "workload blocks",
+                   "partition": ["workload blocks", "balanced", "searched (delay model)"][a.partition],
                    "sync": ["events", "stream values"][a.sync],
                    "parallelism": "none (1 GPU)"},
         "swapped_ms": round(sw_ms, 4), "resident_ms": round(res_ms, 4),
@@ -487,6 +499,14 @@ def main():
         "mfma_util": round(mfma_util, 5) if mfma_util else None,
         "roofline": roofline,
         "timeline": {k: v for k, v in tl.items() if k != "per_slab" or a.verbose},
+        "delay_model": {"link_gbps": round(1e-9 / model["alpha"], 2) if model["alpha"] > 0 else None,
+                        "beta_us": round(model["beta"] * 1e6, 2),
+                        "gate_us": round(model["gate"] * 1e6, 2),
+                        "wake_us": round(model["wake"] * 1e6, 2),
+                        "slab_ex_us": round(model["slab_ex"] * 1e6, 2),
+                        "predicted_latency_ms": round(pred_lat * 1e3, 4),
+                        "predicted_ms_per_step": round(pred_per * 1e3, 4),
+                        "calibrated_on": "workload-block plan" if cm is not None else "this plan"},
         "kernels": {k: {"launches": v[0], "ms": round(v[1], 4)} for k, v in groups.items()},
         "swapped_equals_resident_bitwise": bitwise,
         "activation_bytes": st["activation_bytes"],

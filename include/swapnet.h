@@ -186,7 +186,14 @@ enum sn_option {
                                    m = 2 parallel blocks of equal share),
                                    cutting layers by output channels where a
                                    slab boundary falls inside one; fewer,
-                                   larger DMAs at small budgets               */
+                                   larger DMAs at small budgets; 2: the
+                                   partition with the least predicted time
+                                   per inference under the context's delay
+                                   model (sn_cost_model; Sec. 6, Eq. 4),
+                                   searched over slab counts around
+                                   ceil(2 s / B) and cut points at layer
+                                   boundaries or inside large layers, with
+                                   partitions 0 and 1 as candidates too      */
     SN_OPT_SYNC = 9,            /* copy-thread mode (SN_OPT_SWAPIN 2): how
                                    the copy and compute streams order each
                                    other.  0: hipEvents for "slab loaded" and
@@ -205,6 +212,72 @@ enum sn_option {
                                    SN_OPT_TIMING is on, nor for token nets    */
 };
 int sn_set_option(sn_ctx *ctx, int option, int64_t value);
+
+/* Delay model of a swapped run (Sec. 5: input, execution and output delays
+ * of a block, each linear in the block's bytes, parameter depth or FLOPs,
+ * with device-dependent coefficients).  For this engine, in seconds:
+ *   swap-in of a slab    t_in  = alpha * bytes + beta   (one DMA per slab;
+ *                                 binding parameters by pointer costs the
+ *                                 device nothing, so the paper's depth term
+ *                                 becomes a per-DMA term);
+ *   execution of a slab  t_ex  = slab_ex + sum of its pieces, a piece being
+ *                                 a layer or an output-channel slice of one:
+ *                                 layer time T = layer_ex[l] if given (>= 0),
+ *                                 else gamma * FLOPs + kappa; a slice of
+ *                                 u of U units takes kappa + (T - kappa) u/U;
+ *   swap-out             t_out = 0 (no write-back; the range is reused).
+ * A swap-in starts `gate` after the compute it waits for has finished (and
+ * after the previous DMA); a slab's compute starts `wake` after its swap-in
+ * has finished (and after the previous slab's compute).  The predicted time
+ * of a plan replays this schedule for inferences issued back to back. */
+typedef struct sn_cost_model {
+    double alpha;               /* s per byte swapped in                      */
+    double beta;                /* s per swap-in DMA                          */
+    double gamma;               /* s per FLOP (layers without layer_ex)       */
+    double kappa;               /* s per layer launch (ditto)                 */
+    double gate;                /* s, compute end -> waiting DMA start        */
+    double wake;                /* s, DMA end -> waiting compute start        */
+    double slab_ex;             /* s per slab on the compute stream           */
+    const float *layer_ex;      /* n_layers measured layer times (s; < 0 =
+                                   not measured), or NULL                     */
+    int32_t n_layers;           /* 0, or the number of layers added           */
+} sn_cost_model;
+
+/* Replace the context's delay model (defaults: coefficients measured on one
+ * MI355X, no per-layer times).  Any state; the partition (SN_OPT_PARTITION
+ * 2) is chosen at sn_plan from the model set by then, so per-layer times must
+ * be given after the last sn_add_block.  The context copies layer_ex.
+ * Errors: SN_E_INVALID (negative or non-finite coefficient, layer count
+ * mismatch). */
+int sn_set_cost_model(sn_ctx *ctx, const sn_cost_model *model);
+
+/* Read the context's delay model.  If `layer_ex` is not NULL it must hold
+ * `n_layers` = the number of layers added; it receives the per-layer times
+ * (-1: not measured) and out->layer_ex points to it; else out->layer_ex is
+ * NULL and out->n_layers 0. */
+int sn_get_cost_model(const sn_ctx *ctx, sn_cost_model *out, float *layer_ex, int n_layers);
+
+/* Measure the delay model of this planned context on its device and keep it
+ * (what sn_get_cost_model then returns): X = min(image, budget) bytes of the
+ * image copied into the arena as one DMA and as 16 DMAs with an event after
+ * each (beta = extra time per DMA, alpha = the rest per byte; best of
+ * `reps`), `reps` inferences with per-piece events
+ * (layer_ex, median per layer) and, for a swapped plan, `reps` with per-slab
+ * events (gate, wake, slab_ex); gamma and kappa are kept.  The inferences
+ * run on the staging buffers (image networks, zero input) or with token id 0
+ * at the current position, which is not advanced (token networks: the KV
+ * entry at that position is overwritten; needs position < max_seq).  A
+ * resident arena holds the image at the same offsets, so it keeps its
+ * weights.  Synchronous; waits for earlier inferences first.  reps in
+ * [1, 64].  Errors: SN_E_STATE, SN_E_UNSUPPORTED (host-only), SN_E_INVALID,
+ * SN_E_HIP. */
+int sn_calibrate(sn_ctx *ctx, int reps);
+
+/* Predicted time of the planned context under its delay model: one
+ * inference from an idle start (`latency_s`) and the steady-state time per
+ * inference when inferences are issued back to back (`period_s`).  Host
+ * only (also for host-only contexts).  Errors: SN_E_STATE before sn_plan. */
+int sn_predict(const sn_ctx *ctx, double *latency_s, double *period_s);
 
 /* Image networks.  `input` is the fp16 input in canonical C x H x W order;
  * `output` receives the last layer's output (C x H x W fp16 for spatial

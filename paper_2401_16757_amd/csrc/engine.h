@@ -64,6 +64,13 @@ struct Slab {
                                       // swap-in of this slab waits for it (-1: none)
 };
 
+// Output units [u0, u1) of one layer, before the slab layout is fixed.
+struct PieceSpec {
+    int layer;
+    int64_t u0, u1;
+};
+using SlabSpec = std::vector<PieceSpec>;
+
 struct PlanResult {
     std::vector<Piece> pieces;
     std::vector<Slab> slabs;
@@ -71,13 +78,47 @@ struct PlanResult {
     int64_t image_bytes = 0, high_water = 0;
 };
 
+// Delay model of a slab (the input / execution / output delays of Sec. 5,
+// for this engine; see sn_cost_model in swapnet.h).  Times in seconds.
+struct CostModel {
+    double alpha = 1.0 / 56e9;   // swap-in per byte
+    double beta = 14e-6;         // swap-in per DMA
+    double gamma = 1.0 / 150e12; // execution per FLOP (layers without a measured time)
+    double kappa = 6e-6;         // execution per kernel launch (ditto; also the part
+                                 // of a layer's time a slice of it keeps whole)
+    double gate = 20e-6;         // compute end -> start of the DMA waiting for it
+    double wake = 5e-6;          // DMA end -> start of the compute waiting for it
+    double slab_ex = 6e-6;       // per slab on the compute stream, beyond its layers
+    std::vector<double> layer_ex;   // measured seconds per layer (< 0: not measured)
+};
+
+struct PlanTimes {
+    double latency = 0;   // one inference, from an idle start
+    double period = 0;    // per inference, back to back, steady state
+};
+
 // Host-only planning (no device calls).
 int validate_layers(std::vector<Layer> &layers, int from, std::vector<Slot> &slots,
                     std::string &err);
 int prepack_layer(Layer &L, const uint8_t *blob, size_t blob_bytes, std::string &err);
+// partition: 0 user blocks, 1 balanced, 2 searched under `cost` (sn_option
+// SN_OPT_PARTITION).  `arena_budget` is where the slabs will be placed.
 int plan_slabs(const std::vector<Layer> &layers, int n_blocks, int64_t split_budget,
-               int64_t max_slab, bool balanced, PlanResult &out, std::string &err);
+               int64_t arena_budget, int64_t max_slab, int partition, const CostModel &cost,
+               PlanResult &out, std::string &err);
+void layout_slabs(const std::vector<Layer> &layers, const std::vector<SlabSpec> &specs,
+                  PlanResult &out);
+int64_t spec_bytes(const std::vector<Layer> &layers, const SlabSpec &s);
 int place_slabs(PlanResult &p, int64_t arena_budget, std::string &err);
+double layer_flops(const Layer &L);
+PlanTimes simulate_plan(const std::vector<Layer> &layers, const PlanResult &placed,
+                        const CostModel &cost);
+// The partition with the least predicted steady-state time per inference
+// (then the least latency) among `seeds` and the searched candidates.
+int search_partition(const std::vector<Layer> &layers, int64_t split_budget,
+                     int64_t arena_budget, int64_t max_slab, const CostModel &cost,
+                     const std::vector<std::vector<SlabSpec>> &seeds,
+                     std::vector<SlabSpec> &best, std::string &err);
 void assign_slot_offsets(std::vector<Slot> &slots, int64_t &total);
 void write_image(const std::vector<Layer> &layers, const PlanResult &p, uint8_t *image);
 void choose_kernels(std::vector<Layer> &layers);

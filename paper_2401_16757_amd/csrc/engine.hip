@@ -12,10 +12,13 @@
 //             slab's "loaded" event;
 //   swap-out  recording the slab's "done" event: nothing is freed or written
 //             back, the range is simply reused.
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <atomic>
 #include <chrono>
+#include <cmath>
 #include <condition_variable>
 #include <cstdio>
 #include <memory>
@@ -92,6 +95,7 @@ struct sn_ctx {
     int64_t act_bytes = 0;
     uint8_t *kv = nullptr;
     int partition = 0;                 // SN_OPT_PARTITION
+    CostModel cost;                    // delay model (sn_set_cost_model / sn_calibrate)
     int64_t kv_bytes = 0;
     int64_t attn_ws_bytes = 0;
     int kv_layers = 0, max_seq = 0, d_model = 0, max_tokens = 0;
@@ -137,6 +141,24 @@ static int fail(sn_ctx *c, int code, const std::string &msg) {
 static hipError_t ensure_stream(hipStream_t *s) {
     if (*s) return hipSuccess;
     return hipStreamCreateWithFlags(s, hipStreamNonBlocking);
+}
+
+// A stream with a hardware queue of its own.  The runtime multiplexes
+// ordinary streams over a few in-order hardware queues; a copy stream that
+// shares one with the compute stream queues its "copy done" markers (which
+// wait for the DMA) among the compute kernels, and a kernel behind such a
+// marker waits for a DMA it does not depend on.  A stream created with a
+// CU mask gets a queue of its own; the mask names every CU, so the stream's
+// kernels (the copy kernel of SN_OPT_SWAPIN 0) may still run anywhere.
+static hipError_t ensure_own_queue_stream(hipStream_t *s, int device) {
+    if (*s) return hipSuccess;
+    int cus = 0;
+    hipError_t e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, device);
+    if (e != hipSuccess) return e;
+    if (cus <= 0) return hipErrorInvalidValue;
+    std::vector<uint32_t> mask((cus + 31) / 32, 0u);
+    for (int i = 0; i < cus; ++i) mask[i / 32] |= 1u << (i % 32);
+    return hipExtStreamCreateWithCUMask(s, (uint32_t)mask.size(), mask.data());
 }
 
 #define HIP_TRY(ctx, call)                                                                       \
@@ -243,7 +265,7 @@ extern "C" int sn_set_option(sn_ctx *c, int option, int64_t value) {
         if (value != 1 && value != 2) return fail(c, SN_E_INVALID, "copy streams must be 1 or 2");
         if (c->state == ST_PLANNED && c->have_prev) wait_copier_idle(c);
         if (value == 2 && c->state == ST_PLANNED && !c->host_only && !c->plan.resident)
-            HIP_TRY(c, ensure_stream(&c->copy_s2));
+            HIP_TRY(c, ensure_own_queue_stream(&c->copy_s2, c->device));
         c->copy_streams = (int)value;
         return SN_OK;
     case SN_OPT_MAX_SLAB:
@@ -259,7 +281,7 @@ extern "C" int sn_set_option(sn_ctx *c, int option, int64_t value) {
         return SN_OK;
     case SN_OPT_PARTITION:
         if (c->state != ST_ADDING) return fail(c, SN_E_STATE, "partition is fixed at plan");
-        if (value != 0 && value != 1) return fail(c, SN_E_INVALID, "partition must be 0 or 1");
+        if (value < 0 || value > 2) return fail(c, SN_E_INVALID, "partition must be 0, 1 or 2");
         c->partition = (int)value;
         return SN_OK;
     default:
@@ -290,8 +312,8 @@ extern "C" int sn_plan(sn_ctx *c) {
     const int L = (int)c->layers.size();
     // the network output stays live to the end
     c->slots[c->layers[L - 1].d.dst].last = L;
-    int rc = plan_slabs(c->layers, c->n_blocks, c->split_budget, c->max_slab, c->partition == 1,
-                        c->plan, err);
+    int rc = plan_slabs(c->layers, c->n_blocks, c->split_budget, c->budget, c->max_slab, c->partition,
+                        c->cost, c->plan, err);
     if (rc) return fail(c, rc, err);
     rc = place_slabs(c->plan, c->budget, err);
     if (rc) return fail(c, rc, err);
@@ -414,8 +436,8 @@ extern "C" int sn_plan(sn_ctx *c) {
     c->slab_t_ex_start.assign(ns, 0.f);
 
     if (!c->plan.resident) {
-        HIP_TRY(c, ensure_stream(&c->copy_s));
-        if (c->copy_streams == 2) HIP_TRY(c, ensure_stream(&c->copy_s2));
+        HIP_TRY(c, ensure_own_queue_stream(&c->copy_s, c->device));
+        if (c->copy_streams == 2) HIP_TRY(c, ensure_own_queue_stream(&c->copy_s2, c->device));
         HIP_TRY(c, hipHostMalloc((void **)&c->sig_host, (ns + 1) * sizeof(unsigned long long),
                                  hipHostMallocMapped));
         memset(c->sig_host, 0, (ns + 1) * sizeof(unsigned long long));
@@ -1010,6 +1032,231 @@ extern "C" int sn_reset(sn_ctx *c) {
     if (!c) return SN_E_INVALID;
     if (c->state != ST_PLANNED) return fail(c, SN_E_STATE, "sn_reset before sn_plan");
     c->pos = 0;
+    return SN_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Delay model (Sec. 5): the context's coefficients, their measurement on the
+// device, and the predicted time of the plan.
+// ---------------------------------------------------------------------------
+extern "C" int sn_set_cost_model(sn_ctx *c, const sn_cost_model *m) {
+    if (!c || !m) return SN_E_INVALID;
+    const double v[] = {m->alpha, m->beta, m->gamma, m->kappa, m->gate, m->wake, m->slab_ex};
+    for (double x : v)
+        if (!std::isfinite(x) || x < 0) return fail(c, SN_E_INVALID, "cost coefficients must be finite and >= 0");
+    if (m->n_layers < 0 || (m->n_layers > 0 && !m->layer_ex))
+        return fail(c, SN_E_INVALID, "layer_ex: NULL with n_layers > 0");
+    if (m->n_layers && m->n_layers != (int)c->layers.size())
+        return fail(c, SN_E_INVALID, "layer_ex must have one entry per layer added");
+    CostModel cm;
+    cm.alpha = m->alpha;
+    cm.beta = m->beta;
+    cm.gamma = m->gamma;
+    cm.kappa = m->kappa;
+    cm.gate = m->gate;
+    cm.wake = m->wake;
+    cm.slab_ex = m->slab_ex;
+    for (int l = 0; l < m->n_layers; ++l) {
+        const float t = m->layer_ex[l];
+        cm.layer_ex.push_back(std::isfinite(t) && t >= 0 ? (double)t : -1.0);
+    }
+    c->cost = cm;
+    return SN_OK;
+}
+
+extern "C" int sn_get_cost_model(const sn_ctx *c, sn_cost_model *o, float *layer_ex, int n_layers) {
+    if (!c || !o) return SN_E_INVALID;
+    const CostModel &m = c->cost;
+    memset(o, 0, sizeof(*o));
+    o->alpha = m.alpha;
+    o->beta = m.beta;
+    o->gamma = m.gamma;
+    o->kappa = m.kappa;
+    o->gate = m.gate;
+    o->wake = m.wake;
+    o->slab_ex = m.slab_ex;
+    if (layer_ex) {
+        if (n_layers != (int)c->layers.size()) return SN_E_INVALID;
+        for (int l = 0; l < n_layers; ++l)
+            layer_ex[l] = l < (int)m.layer_ex.size() ? (float)m.layer_ex[l] : -1.f;
+        o->layer_ex = layer_ex;
+        o->n_layers = n_layers;
+    }
+    return SN_OK;
+}
+
+extern "C" int sn_predict(const sn_ctx *c, double *latency_s, double *period_s) {
+    if (!c || !latency_s || !period_s) return SN_E_INVALID;
+    if (c->state != ST_PLANNED) return SN_E_STATE;
+    const PlanTimes t = simulate_plan(c->layers, c->plan, c->cost);
+    *latency_s = t.latency;
+    *period_s = t.period;
+    return SN_OK;
+}
+
+static double median_of(std::vector<double> v) {
+    std::sort(v.begin(), v.end());
+    const size_t n = v.size();
+    return n % 2 ? v[n / 2] : 0.5 * (v[n / 2 - 1] + v[n / 2]);
+}
+
+// One inference for calibration, at the current timing level: the image
+// network on its staging buffers, the token network one token (id 0) at the
+// current position, without advancing it.
+static int calib_run(sn_ctx *c) {
+    int rc;
+    if (c->token) {
+        HIP_TRY(c, hipMemsetAsync(c->d_ids, 0, 4, c->comp_s));
+        if (c->have_prev) HIP_TRY(c, hipStreamWaitEvent(c->comp_s, c->ev_end, 0));
+        auto none = [](hipStream_t) { return (int)SN_OK; };
+        rc = run_slabs(c, 1, c->comp_s, none, none, false);
+        if (!rc) {
+            HIP_TRY(c, hipEventRecord(c->ev_end, c->comp_s));
+            c->have_prev = true;
+        }
+    } else {
+        const int64_t n = c->n_infers;
+        rc = infer_dev_impl(c, c->in_stage, c->out_stage, c->comp_s);
+        c->n_infers = n;
+    }
+    if (rc) {
+        hipStreamSynchronize(c->comp_s);
+        if (c->copy_s) hipStreamSynchronize(c->copy_s);
+        return rc;
+    }
+    HIP_TRY(c, hipStreamSynchronize(c->comp_s));
+    if ((rc = check_copier(c))) return rc;
+    collect_timing(c);
+    return SN_OK;
+}
+
+// Measures the delay model of this context on the device (Sec. 5: the
+// coefficients are profiled once per device; here also per network):
+//  * swap-in: the same bytes moved as one DMA and as 16 DMAs with an event
+//    after each, as the engine issues them (beta = the extra time per DMA,
+//    alpha = the rest per byte);
+//  * execution: per-layer times from per-piece events (timing level 2),
+//    median over `reps` inferences;
+//  * swapped plans only: from per-slab events (timing level 1), `gate` (end
+//    of a compute to the start of the swap-in that waited for it), `wake`
+//    (end of a swap-in to the start of the compute that waited for it) and
+//    `slab_ex` (a slab's compute beyond its layers).
+static int calibrate_impl(sn_ctx *c, int reps, CostModel &m) {
+    HIP_TRY(c, ensure_stream(&c->comp_s));
+    HIP_TRY(c, ensure_own_queue_stream(&c->copy_s, c->device));
+    if (c->copier.joinable()) wait_copier_idle(c);
+    if (c->have_prev) HIP_TRY(c, hipEventSynchronize(c->ev_end));
+    HIP_TRY(c, hipStreamSynchronize(c->comp_s));
+    HIP_TRY(c, hipStreamSynchronize(c->copy_s));
+    if (c->copy_s2) HIP_TRY(c, hipStreamSynchronize(c->copy_s2));
+    if (!c->token) HIP_TRY(c, hipMemsetAsync(c->in_stage, 0, (size_t)c->in_bytes, c->comp_s));
+    const int ns = (int)c->plan.slabs.size();
+    const int np = (int)c->plan.pieces.size();
+    const int L = (int)c->layers.size();
+    hipStream_t q = c->copy_s;
+
+    // swap-in: the first X bytes of the image into the first X bytes of the
+    // arena, once as one DMA and once as 16 DMAs each followed by an event
+    // record (as the engine issues them); the difference is 15 per-DMA
+    // costs.  A resident arena holds the image at the same offsets, so it
+    // keeps its weights.
+    const int64_t X = std::min<int64_t>(c->plan.image_bytes, c->budget) / (16 * kAlign) * (16 * kAlign);
+    if (X > 0) {
+        constexpr int K = 16;
+        const int64_t part = X / K;
+        double t_one = 0, t_many = 0;
+        for (int r = 0; r < reps; ++r) {
+            float ms = 0;
+            HIP_TRY(c, hipEventRecord(c->t_start, q));
+            HIP_TRY(c, hipMemcpyAsync(c->arena, c->image, (size_t)X, hipMemcpyHostToDevice, q));
+            HIP_TRY(c, hipEventRecord(c->t_ex0[0], q));
+            HIP_TRY(c, hipStreamSynchronize(q));
+            HIP_TRY(c, hipEventElapsedTime(&ms, c->t_start, c->t_ex0[0]));
+            t_one = r ? std::min(t_one, ms * 1e-3) : ms * 1e-3;
+            HIP_TRY(c, hipEventRecord(c->t_start, q));
+            for (int k = 0; k < K; ++k) {
+                HIP_TRY(c, hipMemcpyAsync(c->arena + k * part, c->image + k * part, (size_t)part,
+                                          hipMemcpyHostToDevice, q));
+                HIP_TRY(c, hipEventRecord(c->loaded[k % ns], q));
+            }
+            HIP_TRY(c, hipEventRecord(c->t_ex0[0], q));
+            HIP_TRY(c, hipStreamSynchronize(q));
+            HIP_TRY(c, hipEventElapsedTime(&ms, c->t_start, c->t_ex0[0]));
+            t_many = r ? std::min(t_many, ms * 1e-3) : ms * 1e-3;
+        }
+        m.beta = std::max(0.0, (t_many - t_one) / (K - 1));
+        m.alpha = std::max(t_one - m.beta, 0.5 * t_one) / (double)X;
+    }
+
+    // execution: per layer, from per-piece events
+    const int saved = c->timing;
+    std::vector<std::vector<double>> lt(L), pt(np);
+    c->timing = 2;
+    int rc = SN_OK;
+    for (int r = 0; r < reps && !rc; ++r) {
+        if ((rc = calib_run(c))) break;
+        std::vector<double> per(L, 0.0);
+        std::vector<char> seen(L, 0);
+        for (int j = 0; j < np; ++j) {
+            const int l = c->plan.pieces[j].layer;
+            per[l] += c->piece_ms[j] * 1e-3;
+            seen[l] = 1;
+            pt[j].push_back(c->piece_ms[j] * 1e-3);
+        }
+        for (int l = 0; l < L; ++l)
+            if (seen[l]) lt[l].push_back(per[l]);
+    }
+    if (!rc) {
+        m.layer_ex.assign(L, -1.0);
+        for (int l = 0; l < L; ++l)
+            if (!lt[l].empty()) m.layer_ex[l] = median_of(lt[l]);
+    }
+
+    // schedule constants, from per-slab events of swapped inferences
+    if (!rc && !c->plan.resident) {
+        std::vector<double> piece_med(np, 0.0), gate, wake, extra;
+        for (int j = 0; j < np; ++j)
+            if (!pt[j].empty()) piece_med[j] = median_of(pt[j]);
+        c->timing = 1;
+        const double eps = 2e-6;
+        for (int r = 0; r < reps && !rc; ++r) {
+            if ((rc = calib_run(c))) break;
+            auto in0 = [&](int i) { return c->slab_t_in_start[i] * 1e-3; };
+            auto in1 = [&](int i) { return (c->slab_t_in_start[i] + c->slab_t_in[i]) * 1e-3; };
+            auto ex0 = [&](int i) { return c->slab_t_ex_start[i] * 1e-3; };
+            auto ex1 = [&](int i) { return (c->slab_t_ex_start[i] + c->slab_t_ex[i]) * 1e-3; };
+            for (int i = 0; i < ns; ++i) {
+                const Slab &s = c->plan.slabs[i];
+                double pieces = 0;
+                for (int pi : s.pieces) pieces += piece_med[pi];
+                extra.push_back(std::max(0.0, c->slab_t_ex[i] * 1e-3 - pieces));
+                // a swap-in that started after the compute it waited for
+                // and after the DMA queue had drained
+                if (s.wait >= 0 && in0(i) > ex1(s.wait) && (i == 0 || in0(i) > in1(i - 1) + eps))
+                    gate.push_back(in0(i) - ex1(s.wait));
+                // a compute that started after its swap-in, with the
+                // previous slab's compute already finished
+                if (in1(i) > (i ? ex1(i - 1) : 0.0) + eps) wake.push_back(std::max(0.0, ex0(i) - in1(i)));
+            }
+        }
+        if (!rc) {
+            if (!gate.empty()) m.gate = median_of(gate);
+            if (!wake.empty()) m.wake = median_of(wake);
+            if (!extra.empty()) m.slab_ex = median_of(extra);
+        }
+    }
+    c->timing = saved;
+    return rc;
+}
+
+extern "C" int sn_calibrate(sn_ctx *c, int reps) {
+    int rc = check_ready(c, c ? c->token : false);
+    if (rc) return rc;
+    if (reps < 1 || reps > 64) return fail(c, SN_E_INVALID, "reps must be in [1, 64]");
+    if (c->token && c->pos >= c->max_seq) return fail(c, SN_E_INVALID, "KV cache full (max_seq reached)");
+    CostModel m = c->cost;
+    if ((rc = calibrate_impl(c, reps, m))) return rc;
+    c->cost = m;
     return SN_OK;
 }
 

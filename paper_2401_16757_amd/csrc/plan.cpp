@@ -318,11 +318,7 @@ int prepack_layer(Layer &L, const uint8_t *blob, size_t blob_bytes, std::string 
 // Slab lowering
 // ---------------------------------------------------------------------------
 namespace {
-struct PS {  // piece spec during lowering
-    int layer;
-    int64_t u0, u1;
-};
-using SlabSpec = std::vector<PS>;
+using PS = PieceSpec;
 
 int64_t piece_bytes(const std::vector<Layer> &layers, const PS &p) {
     const Layer &L = layers[p.layer];
@@ -490,10 +486,14 @@ static int balanced_slabs(const std::vector<Layer> &layers, int64_t B, int64_t m
     return SN_OK;
 }
 
-int plan_slabs(const std::vector<Layer> &layers, int n_blocks, int64_t split_budget,
-               int64_t max_slab, bool balanced, PlanResult &res, std::string &err) {
-    const int64_t B = split_budget / kAlign * kAlign;
-    std::vector<SlabSpec> slabs(n_blocks);
+int64_t spec_bytes(const std::vector<Layer> &layers, const SlabSpec &s) { return slab_bytes(layers, s); }
+
+// Lowering of partitions 0 and 1: start from the user blocks (0) or the
+// balanced re-cut (1), then split until every slab and every two consecutive
+// slabs fit.
+static int lower_slabs(const std::vector<Layer> &layers, int n_blocks, int64_t B, int64_t max_slab,
+                       bool balanced, std::vector<SlabSpec> &slabs, std::string &err) {
+    slabs.assign(n_blocks, SlabSpec());
     for (int li = 0; li < (int)layers.size(); ++li) {
         const Layer &L = layers[li];
         int64_t u1 = L.units ? L.units : 0;
@@ -544,8 +544,40 @@ int plan_slabs(const std::vector<Layer> &layers, int n_blocks, int64_t split_bud
         slabs.erase(slabs.begin() + j);
         slabs.insert(slabs.begin() + j, parts.begin(), parts.end());
     }
-    // Lay out each slab: every tensor 256-byte aligned, slabs back to back in
-    // the image.
+    return SN_OK;
+}
+
+int plan_slabs(const std::vector<Layer> &layers, int n_blocks, int64_t split_budget,
+               int64_t arena_budget, int64_t max_slab, int partition, const CostModel &cost,
+               PlanResult &res, std::string &err) {
+    const int64_t B = split_budget / kAlign * kAlign;
+    std::vector<SlabSpec> slabs;
+    int rc = lower_slabs(layers, n_blocks, B, max_slab, partition == 1, slabs, err);
+    if (rc) return rc;
+    if (partition == 2) {
+        int64_t total = 0;
+        for (const SlabSpec &ss : slabs) total += slab_bytes(layers, ss);
+        if (total > B) {
+            // the user blocks and the balanced partition compete with the
+            // searched ones
+            std::vector<std::vector<SlabSpec>> seeds{slabs};
+            std::vector<SlabSpec> bal;
+            std::string ignored;
+            if (!lower_slabs(layers, n_blocks, B, max_slab, true, bal, ignored)) seeds.push_back(bal);
+            std::vector<SlabSpec> found;
+            rc = search_partition(layers, B, arena_budget, max_slab, cost, seeds, found, err);
+            if (rc) return rc;
+            slabs.swap(found);
+        }
+    }
+    layout_slabs(layers, slabs, res);
+    return SN_OK;
+}
+
+// Lay out each slab: every tensor 256-byte aligned, slabs back to back in the
+// image.
+void layout_slabs(const std::vector<Layer> &layers, const std::vector<SlabSpec> &slabs,
+                  PlanResult &res) {
     res.pieces.clear();
     res.slabs.clear();
     int64_t image_off = 0;
@@ -578,7 +610,6 @@ int plan_slabs(const std::vector<Layer> &layers, int n_blocks, int64_t split_bud
         res.slabs.push_back(sl);
     }
     res.image_bytes = image_off;
-    return SN_OK;
 }
 
 // Arena placement.  The pair constraint (Eq. 3) guarantees that slab i and

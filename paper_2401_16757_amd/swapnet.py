@@ -33,7 +33,9 @@ OPT_SYNC = 9
 
 EXPORTS = ["sn_create", "sn_create_ex", "sn_add_block", "sn_plan", "sn_set_option", "sn_infer",
            "sn_infer_dev", "sn_infer_tokens", "sn_reset", "sn_get_stats", "sn_get_slab",
-           "sn_get_piece", "sn_get_image", "sn_kernel_name", "sn_last_error", "sn_destroy"]
+           "sn_get_piece", "sn_get_image", "sn_kernel_name", "sn_last_error", "sn_destroy",
+           "sn_set_cost_model", "sn_get_cost_model", "sn_calibrate", "sn_predict"]
+COST_KEYS = ("alpha", "beta", "gamma", "kappa", "gate", "wake", "slab_ex")
 
 
 class SnLayer(C.Structure):
@@ -72,6 +74,11 @@ class SnPieceInfo(C.Structure):
                 ("ksplit", C.c_int32), ("t_main_ms", C.c_float)]
 
 
+class SnCostModel(C.Structure):
+    _fields_ = [(k, C.c_double) for k in COST_KEYS] + \
+               [("layer_ex", C.POINTER(C.c_float)), ("n_layers", C.c_int32)]
+
+
 _lib = None
 
 
@@ -97,6 +104,10 @@ def load_library(path=LIB_PATH):
         "sn_get_piece": (I, [P, I, C.POINTER(SnPieceInfo)]),
         "sn_get_image": (I, [P, C.POINTER(C.c_void_p), C.POINTER(C.c_size_t)]),
         "sn_kernel_name": (C.c_char_p, [I]),
+        "sn_set_cost_model": (I, [P, C.POINTER(SnCostModel)]),
+        "sn_get_cost_model": (I, [P, C.POINTER(SnCostModel), P, I]),
+        "sn_calibrate": (I, [P, I]),
+        "sn_predict": (I, [P, C.POINTER(C.c_double), C.POINTER(C.c_double)]),
         "sn_last_error": (C.c_char_p, [P]), "sn_destroy": (None, [P]),
     }
     for name, (res, args) in sig.items():
@@ -220,6 +231,40 @@ class SwapNet:
             out.append({k: getattr(p, k) for k, _ in SnPieceInfo._fields_})
         return out
 
+    def set_cost_model(self, model):
+        """``model``: dict with the coefficient keys of sn_cost_model (missing
+        ones keep the context's values) and optionally ``layer_ex`` (seconds
+        per layer, < 0 = not measured)."""
+        cur = self.cost_model()
+        m = SnCostModel()
+        for k in COST_KEYS:
+            setattr(m, k, float(model.get(k, cur[k])))
+        ex = model.get("layer_ex")
+        if ex is not None:
+            ex = np.ascontiguousarray(ex, np.float32)
+            m.layer_ex = ex.ctypes.data_as(C.POINTER(C.c_float))
+            m.n_layers = len(ex)
+        return self._check(self.lib.sn_set_cost_model(self.ctx, C.byref(m)))
+
+    def cost_model(self):
+        n = self.stats()["n_layers"]
+        ex = np.zeros(max(n, 1), np.float32)
+        m = SnCostModel()
+        self._check(self.lib.sn_get_cost_model(self.ctx, C.byref(m),
+                                               ex.ctypes.data_as(C.c_void_p) if n else None, n))
+        out = {k: getattr(m, k) for k in COST_KEYS}
+        out["layer_ex"] = ex[:n].copy()
+        return out
+
+    def calibrate(self, reps=3):
+        return self._check(self.lib.sn_calibrate(self.ctx, int(reps)))
+
+    def predict(self):
+        """(latency_s, period_s) of the plan under the context's delay model."""
+        lat, per = C.c_double(), C.c_double()
+        self._check(self.lib.sn_predict(self.ctx, C.byref(lat), C.byref(per)))
+        return lat.value, per.value
+
     def image(self):
         ptr, n = C.c_void_p(), C.c_size_t()
         self._check(self.lib.sn_get_image(self.ctx, C.byref(ptr), C.byref(n)))
@@ -310,9 +355,11 @@ def output_shape(net):
 
 
 def build_engine(net, weights, budget=None, blocks=None, split_budget=None, host_only=False,
-                 timing=False, max_slab=0, partition=0):
+                 timing=False, max_slab=0, partition=0, cost_model=None):
     """Create, register and plan an engine for ``net``.  ``weights`` is a list
-    of per-layer parameter dicts or a callable li -> dict."""
+    of per-layer parameter dicts or a callable li -> dict.  ``cost_model``
+    (a dict as returned by ``SwapNet.cost_model``) is set before planning;
+    with ``partition=2`` it decides the slab partition."""
     eng = SwapNet(budget if budget is not None else net.budget_bytes(), host_only=host_only)
     if split_budget is not None:
         eng.set_option(OPT_SPLIT_BUDGET, split_budget)
@@ -325,6 +372,8 @@ def build_engine(net, weights, budget=None, blocks=None, split_budget=None, host
     for a, b in (blocks or net.blocks):
         descs, blob = block_payload(net, weights, a, b)
         eng.add_block(descs, blob)
+    if cost_model is not None:
+        eng.set_cost_model(cost_model)
     eng.plan()
     eng.out_shape, eng.out_dtype = output_shape(net)
     eng.in_shape = net.input_shape

@@ -172,6 +172,38 @@ def test_balanced_partition_matches_resident(name, kw, frac):
     assert rel_err(y, ref) <= TOL
 
 
+@pytest.mark.parametrize("name,kw,frac", [("resnet50", {"res": 96}, 1 / 5.81),
+                                         ("fcn_resnet101", {"res": 128}, 1 / 4)])
+def test_calibrated_searched_partition_matches_resident(name, kw, frac):
+    # the delay model measured on one plan (sn_calibrate) drives the search
+    # of another (partition 2); calibration leaves its engine computing the
+    # same bits, and the searched plan computes the all-resident bits
+    net, wts, x, ref = net_case(name, **kw)
+    budget = int(net.weight_bytes() * frac)
+    with S.build_engine(net, wts, budget=budget) as cal:
+        y0 = cal.infer(x)
+        cal.calibrate(3)
+        m = cal.cost_model()
+        y1 = cal.infer(x)
+    assert np.array_equal(y0.view(np.uint16), y1.view(np.uint16))
+    assert 10e9 < 1 / m["alpha"] < 100e9 and 0 <= m["beta"] < 200e-6, m
+    assert 0 <= m["gate"] < 1e-3 and 0 <= m["wake"] < 1e-3 and 0 <= m["slab_ex"] < 1e-3, m
+    ex = m["layer_ex"]
+    assert len(ex) == len(net.layers) and np.all(np.isfinite(ex)) and np.all(ex > 0) and ex.sum() < 0.1
+    with S.build_engine(net, wts, budget=budget, partition=2, cost_model=m) as eng:
+        assert not eng.stats()["resident"]
+        y = eng.infer(x)
+        lat, per = eng.predict()
+        assert 0 < per <= lat * 1.01
+    with S.build_engine(net, wts, budget=1 << 33) as res:
+        yr = res.infer(x)
+        res.calibrate(2)   # rewrites the resident arena with its own bytes
+        yr2 = res.infer(x)
+    assert np.array_equal(y.view(np.uint16), yr.view(np.uint16))
+    assert np.array_equal(yr2.view(np.uint16), yr.view(np.uint16))
+    assert rel_err(y, ref) <= TOL
+
+
 @pytest.mark.parametrize("modes", [((2, 0),), ((2, 1),), ((1, 0),), ((0, 0),),
                                    ((2, 1), (1, 0), (2, 0), (0, 0), (2, 1))])
 def test_back_to_back_inferences_with_cross_inference_prefetch(modes):
@@ -237,6 +269,26 @@ def test_decoder_teacher_forced_parity():
             first = got
         else:
             assert np.array_equal(first.view(np.uint32), got.view(np.uint32))
+
+
+def test_decoder_calibration_keeps_generation():
+    # calibrating a token network runs one token at the current position
+    # without advancing it: the generation that follows is unchanged
+    net = small_decoder()
+    wts = W.make_weights(net)
+    prompt = W.make_input(net)
+    lb = sum(l.weight_bytes() for l in net.layers[1:8])
+    runs = []
+    for calibrate in (False, True):
+        with S.build_engine(net, wts, budget=2 * lb) as eng:
+            rows = [eng.infer_tokens(prompt)]
+            if calibrate:
+                eng.calibrate(2)
+                assert np.all(eng.cost_model()["layer_ex"] > 0)
+            for _ in range(4):
+                rows.append(eng.infer_tokens(np.array([int(np.argmax(rows[-1]))], np.int32)))
+            runs.append(np.stack(rows))
+    assert np.array_equal(runs[0].view(np.uint32), runs[1].view(np.uint32))
 
 
 def test_decoder_long_context_split_attention():

@@ -105,7 +105,7 @@ def check_plan(net, eng, budget):
 @pytest.mark.parametrize("name,kw", [("tiny_cnn", {}), ("resnet50", {}), ("vgg16", {}),
                                      ("fcn_resnet101", {})])
 @pytest.mark.parametrize("frac", [None, 1 / 2.32, 1 / 3, 1 / 4, 1 / 5.81])
-@pytest.mark.parametrize("partition", [0, 1])
+@pytest.mark.parametrize("partition", [0, 1, 2])
 def test_plan_invariants(name, kw, frac, partition):
     net = W.get_network(name, **kw)
     budget = net.budget_bytes() if frac is None else int(net.weight_bytes() * frac)
