@@ -17,6 +17,7 @@ Prints ONE JSON line with
 Usage: python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--workload resnet50]
 """
 import argparse
+import gc
 import json
 import os
 import sys
@@ -125,7 +126,17 @@ def measure_copy_chain(torch, sizes, reps=5):
     return best
 
 
+def quiet_gc():
+    """Collect now and move every live object out of the collector's reach:
+    a full collection of this process's objects (torch, numpy, weights)
+    pauses the Python thread for several milliseconds, which would stall the
+    enqueue of whichever inference it lands in."""
+    gc.collect()
+    gc.freeze()
+
+
 def timed_loop(torch, eng, xd, yd, steps, warmup):
+    quiet_gc()
     s = torch.cuda.current_stream()
     for _ in range(warmup):
         eng.infer_dev(xd.data_ptr(), yd.data_ptr(), s.cuda_stream)
@@ -296,6 +307,7 @@ def run_decoder(eng, prompt, gen):
     """Greedy generation: prefill, then gen-1 single-token steps.  Returns
     (prefill_ms, per-step ms list, token ids)."""
     eng.reset()
+    quiet_gc()
     t0 = time.perf_counter()
     logits = eng.infer_tokens(prompt)
     pre = (time.perf_counter() - t0) * 1e3

@@ -258,19 +258,24 @@ int sn_set_cost_model(sn_ctx *ctx, const sn_cost_model *model);
 int sn_get_cost_model(const sn_ctx *ctx, sn_cost_model *out, float *layer_ex, int n_layers);
 
 /* Measure the delay model of this planned context on its device and keep it
- * (what sn_get_cost_model then returns): X = min(image, budget) bytes of the
- * image copied into the arena as one DMA and as 16 DMAs with an event after
- * each (beta = extra time per DMA, alpha = the rest per byte; best of
- * `reps`), `reps` inferences with per-piece events
- * (layer_ex, median per layer) and, for a swapped plan, `reps` with per-slab
- * events (gate, wake, slab_ex); gamma and kappa are kept.  The inferences
- * run on the staging buffers (image networks, zero input) or with token id 0
- * at the current position, which is not advanced (token networks: the KV
- * entry at that position is overwritten; needs position < max_seq).  A
- * resident arena holds the image at the same offsets, so it keeps its
- * weights.  Synchronous; waits for earlier inferences first.  reps in
- * [1, 64].  Errors: SN_E_STATE, SN_E_UNSUPPORTED (host-only), SN_E_INVALID,
- * SN_E_HIP. */
+ * (what sn_get_cost_model then returns; gamma and kappa are kept):
+ *  - alpha, beta: X = min(image, budget) bytes of the image copied into the
+ *    arena as one DMA and as 16 DMAs with an event after each (beta = the
+ *    extra time per DMA, alpha = the rest per byte; best of `reps`);
+ *  - layer_ex: per-piece events (timing level 2), median of `reps`
+ *    inferences; for image networks then scaled, slab by slab, to the time
+ *    of the slab's captured graph replayed without swap-ins, so that they
+ *    include the per-slab overhead (slab_ex is then 0);
+ *  - swapped plans: wake from per-slab events (timing level 1), and gate
+ *    fitted (in [0, 1 ms]) so that the model's time per inference equals the
+ *    measured one for 8 inferences issued back to back.
+ * The inferences run on the staging buffers (image networks, zero input) or
+ * with token id 0 at the current position, which is not advanced (token
+ * networks: the KV entry at that position is overwritten; needs position <
+ * max_seq).  A resident arena holds the image at the same offsets, so it
+ * keeps its weights.  Synchronous; waits for earlier inferences first.  reps
+ * in [1, 64].  Errors: SN_E_STATE, SN_E_UNSUPPORTED (host-only),
+ * SN_E_INVALID, SN_E_HIP. */
 int sn_calibrate(sn_ctx *ctx, int reps);
 
 /* Predicted time of the planned context under its delay model: one

@@ -597,6 +597,16 @@ static int run_piece(sn_ctx *c, int pi, int n_tok, hipStream_t s) {
 // ---------------------------------------------------------------------------
 static inline void cpu_relax() { __builtin_ia32_pause(); }
 
+// One step of a busy wait: a pause for the first iterations, then a yield
+// of the core.  The two threads wait for each other; a woken copy thread may
+// be queued on the core where the calling thread spins, and a wait that
+// never yields would keep it off that core for a whole scheduler slice
+// (milliseconds).
+static inline void spin_step(uint32_t &k) {
+    if (++k < 2048) cpu_relax();
+    else std::this_thread::yield();
+}
+
 static void copier_main(sn_ctx *c) {
     const int ns = (int)c->plan.slabs.size();
     for (;;) {
@@ -609,7 +619,7 @@ static void copier_main(sn_ctx *c) {
                 have = true;
                 break;
             }
-            for (int k = 0; k < 32; ++k) cpu_relax();
+            std::this_thread::yield();
         }
         {
             std::unique_lock<std::mutex> lk(c->mu);
@@ -635,12 +645,13 @@ static void copier_main(sn_ctx *c) {
             const int gi = s.wait >= 0 ? s.wait : (wrap ? s.wrap : ns);
             const uint64_t need = exclusive ? 0 : (wrap ? seq - 1 : seq);
             volatile unsigned long long *gate = c->sig_host + gi;
+            uint32_t k = 0;
             while (*gate < need) {
                 if (c->abort_seq.load() >= seq) {
                     aborted = true;
                     break;
                 }
-                cpu_relax();
+                spin_step(k);
             }
             if (aborted) break;
             hipError_t e = hipSuccess;
@@ -666,7 +677,8 @@ static void copier_main(sn_ctx *c) {
 
 static void wait_copier_idle(sn_ctx *c) {
     if (!c->copier.joinable()) return;
-    while (c->handled.load() < c->tseq) cpu_relax();
+    uint32_t k = 0;
+    while (c->handled.load() < c->tseq) spin_step(k);
 }
 
 // After a synchronous inference: a swap-in the copy thread failed to issue.
@@ -801,7 +813,8 @@ static int run_slabs(sn_ctx *c, int n_tok, hipStream_t cs, Pre pre, Post post, b
         // hardware queues, where a wait enqueued ahead of its producer would
         // block that producer for good
         if (threaded) {
-            while (c->loaded_seq[i].load(std::memory_order_acquire) < seq) cpu_relax();
+            uint32_t k = 0;
+            while (c->loaded_seq[i].load(std::memory_order_acquire) < seq) spin_step(k);
             if (c->copy_error.load()) return abort_copies(fail(c, SN_E_HIP, c->copy_err));
         }
         hipError_t e = hipSuccess;
@@ -1102,8 +1115,8 @@ static double median_of(std::vector<double> v) {
 
 // One inference for calibration, at the current timing level: the image
 // network on its staging buffers, the token network one token (id 0) at the
-// current position, without advancing it.
-static int calib_run(sn_ctx *c) {
+// current position, without advancing it.  calib_enqueue only enqueues it.
+static int calib_enqueue(sn_ctx *c) {
     int rc;
     if (c->token) {
         HIP_TRY(c, hipMemsetAsync(c->d_ids, 0, 4, c->comp_s));
@@ -1122,8 +1135,13 @@ static int calib_run(sn_ctx *c) {
     if (rc) {
         hipStreamSynchronize(c->comp_s);
         if (c->copy_s) hipStreamSynchronize(c->copy_s);
-        return rc;
     }
+    return rc;
+}
+
+static int calib_run(sn_ctx *c) {
+    int rc = calib_enqueue(c);
+    if (rc) return rc;
     HIP_TRY(c, hipStreamSynchronize(c->comp_s));
     if ((rc = check_copier(c))) return rc;
     collect_timing(c);
@@ -1131,16 +1149,11 @@ static int calib_run(sn_ctx *c) {
 }
 
 // Measures the delay model of this context on the device (Sec. 5: the
-// coefficients are profiled once per device; here also per network):
-//  * swap-in: the same bytes moved as one DMA and as 16 DMAs with an event
-//    after each, as the engine issues them (beta = the extra time per DMA,
-//    alpha = the rest per byte);
-//  * execution: per-layer times from per-piece events (timing level 2),
-//    median over `reps` inferences;
-//  * swapped plans only: from per-slab events (timing level 1), `gate` (end
-//    of a compute to the start of the swap-in that waited for it), `wake`
-//    (end of a swap-in to the start of the compute that waited for it) and
-//    `slab_ex` (a slab's compute beyond its layers).
+// coefficients are profiled once per device; here also per network): the
+// link (alpha, beta) from one DMA against 16, the layers from per-piece
+// events scaled to the slab graphs' own times, the wake latency from
+// per-slab events, and the gate latency fitted to the measured time per
+// inference of this plan.  The steps are described with sn_calibrate.
 static int calibrate_impl(sn_ctx *c, int reps, CostModel &m) {
     HIP_TRY(c, ensure_stream(&c->comp_s));
     HIP_TRY(c, ensure_own_queue_stream(&c->copy_s, c->device));
@@ -1212,40 +1225,111 @@ static int calibrate_impl(sn_ctx *c, int reps, CostModel &m) {
             if (!lt[l].empty()) m.layer_ex[l] = median_of(lt[l]);
     }
 
-    // schedule constants, from per-slab events of swapped inferences
+    std::vector<double> piece_med(np, 0.0);
+    for (int j = 0; j < np; ++j)
+        if (!pt[j].empty()) piece_med[j] = median_of(pt[j]);
+
+    // wake, from per-slab events of swapped inferences (timing level 1): the
+    // end of a swap-in to the start of the compute that waited for it
     if (!rc && !c->plan.resident) {
-        std::vector<double> piece_med(np, 0.0), gate, wake, extra;
-        for (int j = 0; j < np; ++j)
-            if (!pt[j].empty()) piece_med[j] = median_of(pt[j]);
+        std::vector<double> wake;
         c->timing = 1;
-        const double eps = 2e-6;
         for (int r = 0; r < reps && !rc; ++r) {
             if ((rc = calib_run(c))) break;
-            auto in0 = [&](int i) { return c->slab_t_in_start[i] * 1e-3; };
-            auto in1 = [&](int i) { return (c->slab_t_in_start[i] + c->slab_t_in[i]) * 1e-3; };
-            auto ex0 = [&](int i) { return c->slab_t_ex_start[i] * 1e-3; };
-            auto ex1 = [&](int i) { return (c->slab_t_ex_start[i] + c->slab_t_ex[i]) * 1e-3; };
             for (int i = 0; i < ns; ++i) {
-                const Slab &s = c->plan.slabs[i];
-                double pieces = 0;
-                for (int pi : s.pieces) pieces += piece_med[pi];
-                extra.push_back(std::max(0.0, c->slab_t_ex[i] * 1e-3 - pieces));
-                // a swap-in that started after the compute it waited for
-                // and after the DMA queue had drained
-                if (s.wait >= 0 && in0(i) > ex1(s.wait) && (i == 0 || in0(i) > in1(i - 1) + eps))
-                    gate.push_back(in0(i) - ex1(s.wait));
-                // a compute that started after its swap-in, with the
-                // previous slab's compute already finished
-                if (in1(i) > (i ? ex1(i - 1) : 0.0) + eps) wake.push_back(std::max(0.0, ex0(i) - in1(i)));
+                const double in1 = (c->slab_t_in_start[i] + c->slab_t_in[i]) * 1e-3;
+                const double ex0 = c->slab_t_ex_start[i] * 1e-3;
+                const double prev = i ? (c->slab_t_ex_start[i - 1] + c->slab_t_ex[i - 1]) * 1e-3 : 0.0;
+                if (in1 > prev + 2e-6) wake.push_back(std::max(0.0, ex0 - in1));
             }
         }
-        if (!rc) {
-            if (!gate.empty()) m.gate = median_of(gate);
-            if (!wake.empty()) m.wake = median_of(wake);
-            if (!extra.empty()) m.slab_ex = median_of(extra);
-        }
+        if (!rc && !wake.empty()) m.wake = median_of(wake);
     }
     c->timing = saved;
+
+    // Execution as the engine runs it.  Image networks: the captured slab
+    // graphs back to back without swap-ins (the arena holds whatever was
+    // loaded last; only the timing is used), one event pair per slab.  The
+    // layer times of each slab are scaled to add up to its graph time, so
+    // the per-slab overhead (launch, signal) is carried by its layers.
+    if (!rc && !c->token && c->use_graph) {
+        if (c->graphs.empty() || c->g_in != c->in_stage || c->g_out != c->out_stage)
+            rc = capture_graphs(c, c->in_stage, c->out_stage);
+        std::vector<double> gt(ns, 1e30);
+        for (int r = 0; r < reps && !rc; ++r) {
+            for (int i = 0; i < ns; ++i) {
+                HIP_TRY(c, hipEventRecord(c->t_ex0[i], c->comp_s));
+                HIP_TRY(c, hipGraphLaunch(c->graphs[i], c->comp_s));
+                HIP_TRY(c, hipEventRecord(c->t_ex1[i], c->comp_s));
+            }
+            HIP_TRY(c, hipStreamSynchronize(c->comp_s));
+            for (int i = 0; i < ns; ++i) {
+                float ms = 0;
+                HIP_TRY(c, hipEventElapsedTime(&ms, c->t_ex0[i], c->t_ex1[i]));
+                gt[i] = std::min(gt[i], ms * 1e-3);
+            }
+        }
+        // the graphs' signal kernels (SN_OPT_SYNC 0) counted slab
+        // completions that belong to no inference: after a complete
+        // inference every counter equals the copy-thread inference count
+        if (c->sig_host)
+            for (int i = 0; i < ns; ++i) ((volatile unsigned long long *)c->sig_host)[i] = c->tseq;
+        if (!rc) {
+            std::vector<double> lex(L, 0.0);
+            std::vector<char> seen(L, 0);
+            for (int i = 0; i < ns; ++i) {
+                double sum = 0;
+                for (int pi : c->plan.slabs[i].pieces) sum += piece_med[pi];
+                const int cnt = (int)c->plan.slabs[i].pieces.size();
+                for (int pi : c->plan.slabs[i].pieces) {
+                    const int l = c->plan.pieces[pi].layer;
+                    lex[l] += sum > 0 ? gt[i] * piece_med[pi] / sum : gt[i] / std::max(cnt, 1);
+                    seen[l] = 1;
+                }
+            }
+            for (int l = 0; l < L; ++l)
+                if (seen[l]) m.layer_ex[l] = lex[l];
+            m.slab_ex = 0;
+        }
+    }
+
+    // gate: the one latency left, fitted so that the model reproduces the
+    // measured time per inference of this plan, back to back
+    if (!rc && !c->plan.resident) {
+        const int K = 8;
+        for (int w = 0; w < 2 && !rc; ++w) rc = calib_enqueue(c);
+        if (!rc) HIP_TRY(c, hipStreamSynchronize(c->comp_s));
+        if (!rc) HIP_TRY(c, hipEventRecord(c->t_start, c->comp_s));
+        for (int k = 0; k < K && !rc; ++k) rc = calib_enqueue(c);
+        if (!rc) {
+            HIP_TRY(c, hipEventRecord(c->t_ex0[0], c->comp_s));
+            HIP_TRY(c, hipStreamSynchronize(c->comp_s));
+            rc = check_copier(c);
+        }
+        if (!rc) {
+            float ms = 0;
+            HIP_TRY(c, hipEventElapsedTime(&ms, c->t_start, c->t_ex0[0]));
+            const double P = ms * 1e-3 / K;
+            auto period_at = [&](double g) {
+                CostModel t = m;
+                t.gate = g;
+                return simulate_plan(c->layers, c->plan, t).period;
+            };
+            double lo = 0, hi = 1e-3;
+            if (period_at(lo) >= P) {
+                m.gate = 0;
+            } else if (period_at(hi) <= P) {
+                m.gate = hi;
+            } else {
+                for (int it = 0; it < 40; ++it) {
+                    const double mid = 0.5 * (lo + hi);
+                    if (period_at(mid) < P) lo = mid;
+                    else hi = mid;
+                }
+                m.gate = 0.5 * (lo + hi);
+            }
+        }
+    }
     return rc;
 }
 
