@@ -51,10 +51,12 @@ def parse():
     ap.add_argument("--no-graph", action="store_true", help="enqueue call by call (no HIP graph)")
     ap.add_argument("--swapin", type=int, default=2, choices=[0, 1, 2],
                     help="0 copy kernel, 1 SDMA from the calling thread, 2 SDMA from the copy thread")
-    ap.add_argument("--partition", type=int, default=0, choices=[0, 1, 2],
+    ap.add_argument("--partition", type=int, default=3, choices=[0, 1, 2, 3],
                     help="0: slabs follow the workload's blocks; 1: balanced re-cut into "
                          "ceil(2 s / B) equal slabs; 2: searched under a delay model "
-                         "calibrated on this GPU (on the workload-block plan, untimed)")
+                         "calibrated on this GPU (on the workload-block plan, untimed); "
+                         "3 (default): the fastest of 0, 1, 2 measured on this GPU "
+                         "(sn_tune, untimed)")
     ap.add_argument("--sync", type=int, default=0, choices=[0, 1],
                     help="copy thread ordering: 0 events + signal kernels, "
                          "1 stream write/wait of values in mapped memory")
@@ -124,6 +126,16 @@ def measure_copy_chain(torch, sizes, reps=5):
             best = t if best is None else min(best, t)
     del h, d
     return best
+
+
+PARTITIONS = ("workload blocks", "balanced", "searched (delay model)")
+
+
+def partition_name(choice, tuned):
+    if tuned is None:
+        return PARTITIONS[choice]
+    best = min((t, i) for i, t in enumerate(tuned) if t)[1]
+    return "tuned: " + PARTITIONS[best]
 
 
 def quiet_gc():
@@ -402,7 +414,12 @@ def main():
             cal.calibrate(5)
             cm = cal.cost_model()
     log("planning swapped engine (budget %d B) and resident engine" % budget)
-    eng_sw = S.build_engine(net, wts, budget=budget, partition=a.partition, cost_model=cm)
+    eng_sw = S.build_engine(net, wts, budget=budget, partition=min(a.partition, 2), cost_model=cm)
+    tuned = None
+    if a.partition == 3:
+        log("choosing the partition by measurement (untimed)")
+        tuned = eng_sw.tune(5)
+        cm = eng_sw.cost_model()
     st = eng_sw.stats()
     eng_res = S.build_engine(net, wts, budget=st["image_bytes"] + 4096)
     eng_sw.set_option(S.OPT_SWAPIN, a.swapin)
@@ -491,7 +508,7 @@ def main():
                    "weight_bytes": net.weight_bytes(), "budget_bytes": budget,
                    "budget_fraction": frac_txt, "user_blocks": len(net.blocks),
                    "slabs": st["n_slabs"],
-                   "partition": ["workload blocks", "balanced", "searched (delay model)"][a.partition],
+                   "partition": partition_name(a.partition, tuned),
                    "sync": ["events", "stream values"][a.sync],
                    "parallelism": "none (1 GPU)"},
         "swapped_ms": round(sw_ms, 4), "resident_ms": round(res_ms, 4),
@@ -518,9 +535,11 @@ def main():
                         "slab_ex_us": round(model["slab_ex"] * 1e6, 2),
                         "predicted_latency_ms": round(pred_lat * 1e3, 4),
                         "predicted_ms_per_step": round(pred_per * 1e3, 4),
-                        "calibrated_on": "workload-block plan" if cm is not None else "this plan"},
+                        "calibrated_on": "this plan" if cm is None else "workload-block plan"},
         "kernels": {k: {"launches": v[0], "ms": round(v[1], 4)} for k, v in groups.items()},
         "swapped_equals_resident_bitwise": bitwise,
+        "partition_candidates_ms": None if tuned is None else
+            {n: round(t * 1e3, 4) if t else None for n, t in zip(PARTITIONS, tuned)},
         "activation_bytes": st["activation_bytes"],
         "hip_graph": not a.no_graph,
         "swapin_mode": {0: "copy kernel", 1: "SDMA, calling thread", 2: "SDMA, copy thread"}[a.swapin],

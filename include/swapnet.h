@@ -148,7 +148,24 @@ int sn_add_block(sn_ctx *ctx, const sn_layer *layers, int n_layers,
  * all-resident.  Errors: SN_E_INFEASIBLE, SN_E_NOMEM, SN_E_HIP, SN_E_STATE. */
 int sn_plan(sn_ctx *ctx);
 
-/* Options (set before sn_plan unless noted). */
+/* Re-plan a planned context in place for a new budget (`budget_bytes`; 0 =
+ * keep the budget) and the current options (SN_OPT_PARTITION,
+ * SN_OPT_MAX_SLAB, SN_OPT_SPLIT_BUDGET if it was set, else the new budget,
+ * and the delay model), without registering the network again: Sec. 6
+ * re-forms blocks from the layers extracted at registration.  The layers'
+ * device-layout tensors are gathered from the pinned image and written to a
+ * new image in the new slab order; activations, the KV cache and the token
+ * position are kept, so a token network continues where it was.  A budget
+ * above the arena's allocation allocates a larger arena.  Waits for earlier
+ * inferences first.  Errors: SN_E_STATE (before sn_plan), SN_E_INVALID,
+ * SN_E_INFEASIBLE and SN_E_NOMEM leave the context as it was; SN_E_HIP
+ * after the old plan was released leaves it unusable (only sn_destroy and
+ * the introspection calls remain). */
+int sn_replan(sn_ctx *ctx, size_t budget_bytes);
+
+/* Options (set before sn_plan unless noted; SN_OPT_SPLIT_BUDGET,
+ * SN_OPT_MAX_SLAB and SN_OPT_PARTITION may also be set later and take
+ * effect at the next sn_replan). */
 enum sn_option {
     SN_OPT_SPLIT_BUDGET = 1,    /* budget used for slab lowering (default: the
                                    arena budget).  With an arena >= image and
@@ -277,6 +294,17 @@ int sn_get_cost_model(const sn_ctx *ctx, sn_cost_model *out, float *layer_ex, in
  * in [1, 64].  Errors: SN_E_STATE, SN_E_UNSUPPORTED (host-only),
  * SN_E_INVALID, SN_E_HIP. */
 int sn_calibrate(sn_ctx *ctx, int reps);
+
+/* Choose the partition by measurement: calibrate the delay model on the
+ * current plan (as sn_calibrate), then plan the context in place
+ * (sn_replan) with each of SN_OPT_PARTITION 0, 1 and 2 (the last searched
+ * under the fresh model), time 8 inferences issued back to back for each
+ * (best of max(1, reps / 2) rounds) and keep the fastest; SN_OPT_PARTITION
+ * is left at the chosen value.  `times_s` (NULL or 3 doubles) receives the
+ * measured seconds per inference of partitions 0, 1, 2 (0: infeasible).  A
+ * resident plan is left as it is.  Runs inferences as sn_calibrate does.
+ * Errors: as sn_calibrate and sn_replan. */
+int sn_tune(sn_ctx *ctx, int reps, double *times_s);
 
 /* Predicted time of the planned context under its delay model: one
  * inference from an idle start (`latency_s`) and the steady-state time per

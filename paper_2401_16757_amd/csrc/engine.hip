@@ -34,7 +34,7 @@
 
 using namespace sn;
 
-enum { ST_ADDING = 0, ST_PLANNED = 1 };
+enum { ST_ADDING = 0, ST_PLANNED = 1, ST_FAILED = 2 };  // FAILED: a re-plan failed midway
 
 struct sn_ctx {
     int64_t budget = 0;
@@ -47,6 +47,8 @@ struct sn_ctx {
     int n_blocks = 0;
     bool token = false;
     int64_t split_budget = 0, max_slab = 0;
+    bool split_explicit = false;       // SN_OPT_SPLIT_BUDGET was set
+    int64_t arena_bytes = 0;           // size of the arena allocation
     int timing = 0;                    // 1: per slab, 2: also per piece
 
     PlanResult plan;
@@ -131,6 +133,7 @@ static thread_local std::string g_create_err;
 static void wait_copier_idle(sn_ctx *c);
 static void drop_graphs(sn_ctx *c);
 static void start_copier(sn_ctx *c);
+static void start_copier(sn_ctx *c);
 static void stop_copier(sn_ctx *c);
 
 static int fail(sn_ctx *c, int code, const std::string &msg) {
@@ -187,6 +190,7 @@ extern "C" sn_ctx *sn_create_ex(size_t budget_bytes, int flags) {
     if (!c->host_only) {
         hipError_t e = hipGetDevice(&c->device);
         if (e == hipSuccess) e = hipMalloc((void **)&c->arena, (size_t)c->budget);
+        if (e == hipSuccess) c->arena_bytes = c->budget;
         // streams are created when first needed: every stream takes one of
         // the process's few hardware queues, and queues shared between a copy
         // stream and a compute stream serialise them
@@ -240,9 +244,9 @@ extern "C" int sn_set_option(sn_ctx *c, int option, int64_t value) {
     if (!c) return SN_E_INVALID;
     switch (option) {
     case SN_OPT_SPLIT_BUDGET:
-        if (c->state != ST_ADDING) return fail(c, SN_E_STATE, "split budget is fixed at plan");
         if (value < kAlign) return fail(c, SN_E_INVALID, "split budget too small");
         c->split_budget = value;
+        c->split_explicit = true;
         return SN_OK;
     case SN_OPT_TIMING:
         if (value < 0 || value > 2) return fail(c, SN_E_INVALID, "timing level must be 0, 1 or 2");
@@ -269,7 +273,6 @@ extern "C" int sn_set_option(sn_ctx *c, int option, int64_t value) {
         c->copy_streams = (int)value;
         return SN_OK;
     case SN_OPT_MAX_SLAB:
-        if (c->state != ST_ADDING) return fail(c, SN_E_STATE, "max slab is fixed at plan");
         if (value < 0) return fail(c, SN_E_INVALID, "negative max slab");
         c->max_slab = value;
         return SN_OK;
@@ -280,7 +283,6 @@ extern "C" int sn_set_option(sn_ctx *c, int option, int64_t value) {
         c->sync = (int)value;
         return SN_OK;
     case SN_OPT_PARTITION:
-        if (c->state != ST_ADDING) return fail(c, SN_E_STATE, "partition is fixed at plan");
         if (value < 0 || value > 2) return fail(c, SN_E_INVALID, "partition must be 0, 1 or 2");
         c->partition = (int)value;
         return SN_OK;
@@ -303,6 +305,109 @@ static void choose_layer_kernels(sn_ctx *c) {
 }
 
 static uint8_t *slot_ptr(sn_ctx *c, int id) { return c->act + c->slots[id].off; }
+
+// Everything that depends on the slab partition: the binding table
+// (assembly by reference: parameter pointers into the arena), per-slab and
+// per-piece events, the copy thread and its counters, and for a resident
+// plan the one upload.
+static int setup_plan_resources(sn_ctx *c) {
+    // binding table (assembly by reference): parameter pointers into the arena
+    const int np = (int)c->plan.pieces.size();
+    c->piece_w.assign(np, nullptr);
+    c->piece_b.assign(np, nullptr);
+    for (const Slab &s : c->plan.slabs)
+        for (int pi : s.pieces) {
+            const Piece &p = c->plan.pieces[pi];
+            if (p.w_bytes) c->piece_w[pi] = c->arena + s.arena_off + p.w_off;
+            if (p.b_bytes) c->piece_b[pi] = c->arena + s.arena_off + p.b_off;
+        }
+
+    const int ns = (int)c->plan.slabs.size();
+    c->loaded.assign(ns, nullptr);
+    c->done.assign(ns, nullptr);
+    for (int i = 0; i < ns; ++i) {
+        HIP_TRY(c, hipEventCreateWithFlags(&c->loaded[i], hipEventDisableTiming));
+        HIP_TRY(c, hipEventCreateWithFlags(&c->done[i], hipEventDisableTiming));
+    }
+    c->t_in0.assign(ns, nullptr);
+    c->t_in1.assign(ns, nullptr);
+    c->t_ex0.assign(ns, nullptr);
+    c->t_ex1.assign(ns, nullptr);
+    for (int i = 0; i < ns; ++i) {
+        HIP_TRY(c, hipEventCreate(&c->t_in0[i]));
+        HIP_TRY(c, hipEventCreate(&c->t_in1[i]));
+        HIP_TRY(c, hipEventCreate(&c->t_ex0[i]));
+        HIP_TRY(c, hipEventCreate(&c->t_ex1[i]));
+    }
+    HIP_TRY(c, hipEventCreate(&c->t_start));
+    HIP_TRY(c, hipEventCreateWithFlags(&c->fork, hipEventDisableTiming));
+    c->t_p0.assign(np, nullptr);
+    c->t_p1.assign(np, nullptr);
+    c->t_pm.assign(np, nullptr);
+    for (int j = 0; j < np; ++j) {
+        HIP_TRY(c, hipEventCreate(&c->t_p0[j]));
+        HIP_TRY(c, hipEventCreate(&c->t_p1[j]));
+        HIP_TRY(c, hipEventCreate(&c->t_pm[j]));
+    }
+    c->piece_ms.assign(np, 0.f);
+    c->piece_main_ms.assign(np, 0.f);
+    c->slab_t_in.assign(ns, 0.f);
+    c->slab_t_ex.assign(ns, 0.f);
+    c->slab_t_in_start.assign(ns, 0.f);
+    c->slab_t_ex_start.assign(ns, 0.f);
+
+    if (!c->plan.resident) {
+        HIP_TRY(c, ensure_own_queue_stream(&c->copy_s, c->device));
+        if (c->copy_streams == 2) HIP_TRY(c, ensure_own_queue_stream(&c->copy_s2, c->device));
+        HIP_TRY(c, hipHostMalloc((void **)&c->sig_host, (ns + 1) * sizeof(unsigned long long),
+                                 hipHostMallocMapped));
+        memset(c->sig_host, 0, (ns + 1) * sizeof(unsigned long long));
+        HIP_TRY(c, hipHostGetDevicePointer((void **)&c->sig_dev, c->sig_host, 0));
+        HIP_TRY(c, hipHostMalloc((void **)&c->lflag_host, ns * sizeof(unsigned long long),
+                                 hipHostMallocMapped));
+        memset(c->lflag_host, 0, ns * sizeof(unsigned long long));
+        HIP_TRY(c, hipHostGetDevicePointer((void **)&c->lflag_dev, c->lflag_host, 0));
+        start_copier(c);
+    }
+    if (c->plan.resident) {
+        // everything fits: one upload now, no swapping per inference
+        for (const Slab &s : c->plan.slabs)
+            if (s.bytes)
+                HIP_TRY(c, hipMemcpy(c->arena + s.arena_off, c->image + s.image_off,
+                                     (size_t)s.bytes, hipMemcpyHostToDevice));
+    }
+    return SN_OK;
+}
+
+// Releases what setup_plan_resources made (no inference may be in flight)
+// and resets the copy thread's bookkeeping.
+static void release_plan_resources(sn_ctx *c) {
+    stop_copier(c);
+    drop_graphs(c);
+    for (auto *v : {&c->loaded, &c->done, &c->t_in0, &c->t_in1, &c->t_ex0, &c->t_ex1, &c->t_p0,
+                    &c->t_p1, &c->t_pm}) {
+        for (hipEvent_t e : *v)
+            if (e) hipEventDestroy(e);
+        v->clear();
+    }
+    if (c->t_start) hipEventDestroy(c->t_start);
+    if (c->fork) hipEventDestroy(c->fork);
+    c->t_start = c->fork = nullptr;
+    if (c->sig_host) hipHostFree(c->sig_host);
+    if (c->lflag_host) hipHostFree(c->lflag_host);
+    c->sig_host = c->sig_dev = c->lflag_host = c->lflag_dev = nullptr;
+    c->stop = false;
+    c->requested = 0;
+    c->seq = c->tseq = 0;
+    c->handled.store(0);
+    c->fork_seq.store(0);
+    c->abort_seq.store(0);
+    c->complete_seq.store(0);
+    c->wrap_ok.store(false);
+    c->wrap_ok_nt = false;
+    c->prev_threaded = true;
+    c->copy_error.store(0);
+}
 
 extern "C" int sn_plan(sn_ctx *c) {
     if (!c) return SN_E_INVALID;
@@ -389,72 +494,8 @@ extern "C" int sn_plan(sn_ctx *c) {
         std::vector<uint16_t>().swap(Ly.b_dev);
     }
 
-    // binding table (assembly by reference): parameter pointers into the arena
-    const int np = (int)c->plan.pieces.size();
-    c->piece_w.assign(np, nullptr);
-    c->piece_b.assign(np, nullptr);
-    for (const Slab &s : c->plan.slabs)
-        for (int pi : s.pieces) {
-            const Piece &p = c->plan.pieces[pi];
-            if (p.w_bytes) c->piece_w[pi] = c->arena + s.arena_off + p.w_off;
-            if (p.b_bytes) c->piece_b[pi] = c->arena + s.arena_off + p.b_off;
-        }
-
-    const int ns = (int)c->plan.slabs.size();
-    c->loaded.assign(ns, nullptr);
-    c->done.assign(ns, nullptr);
-    for (int i = 0; i < ns; ++i) {
-        HIP_TRY(c, hipEventCreateWithFlags(&c->loaded[i], hipEventDisableTiming));
-        HIP_TRY(c, hipEventCreateWithFlags(&c->done[i], hipEventDisableTiming));
-    }
-    c->t_in0.assign(ns, nullptr);
-    c->t_in1.assign(ns, nullptr);
-    c->t_ex0.assign(ns, nullptr);
-    c->t_ex1.assign(ns, nullptr);
-    for (int i = 0; i < ns; ++i) {
-        HIP_TRY(c, hipEventCreate(&c->t_in0[i]));
-        HIP_TRY(c, hipEventCreate(&c->t_in1[i]));
-        HIP_TRY(c, hipEventCreate(&c->t_ex0[i]));
-        HIP_TRY(c, hipEventCreate(&c->t_ex1[i]));
-    }
-    HIP_TRY(c, hipEventCreate(&c->t_start));
-    HIP_TRY(c, hipEventCreateWithFlags(&c->fork, hipEventDisableTiming));
     HIP_TRY(c, hipEventCreateWithFlags(&c->ev_end, hipEventDisableTiming));
-    c->t_p0.assign(np, nullptr);
-    c->t_p1.assign(np, nullptr);
-    c->t_pm.assign(np, nullptr);
-    for (int j = 0; j < np; ++j) {
-        HIP_TRY(c, hipEventCreate(&c->t_p0[j]));
-        HIP_TRY(c, hipEventCreate(&c->t_p1[j]));
-        HIP_TRY(c, hipEventCreate(&c->t_pm[j]));
-    }
-    c->piece_ms.assign(np, 0.f);
-    c->piece_main_ms.assign(np, 0.f);
-    c->slab_t_in.assign(ns, 0.f);
-    c->slab_t_ex.assign(ns, 0.f);
-    c->slab_t_in_start.assign(ns, 0.f);
-    c->slab_t_ex_start.assign(ns, 0.f);
-
-    if (!c->plan.resident) {
-        HIP_TRY(c, ensure_own_queue_stream(&c->copy_s, c->device));
-        if (c->copy_streams == 2) HIP_TRY(c, ensure_own_queue_stream(&c->copy_s2, c->device));
-        HIP_TRY(c, hipHostMalloc((void **)&c->sig_host, (ns + 1) * sizeof(unsigned long long),
-                                 hipHostMallocMapped));
-        memset(c->sig_host, 0, (ns + 1) * sizeof(unsigned long long));
-        HIP_TRY(c, hipHostGetDevicePointer((void **)&c->sig_dev, c->sig_host, 0));
-        HIP_TRY(c, hipHostMalloc((void **)&c->lflag_host, ns * sizeof(unsigned long long),
-                                 hipHostMallocMapped));
-        memset(c->lflag_host, 0, ns * sizeof(unsigned long long));
-        HIP_TRY(c, hipHostGetDevicePointer((void **)&c->lflag_dev, c->lflag_host, 0));
-        start_copier(c);
-    }
-    if (c->plan.resident) {
-        // everything fits: one upload now, no swapping per inference
-        for (const Slab &s : c->plan.slabs)
-            if (s.bytes)
-                HIP_TRY(c, hipMemcpy(c->arena + s.arena_off, c->image + s.image_off,
-                                     (size_t)s.bytes, hipMemcpyHostToDevice));
-    }
+    if ((rc = setup_plan_resources(c))) return rc;
     c->state = ST_PLANNED;
     return SN_OK;
 }
@@ -878,6 +919,7 @@ static void collect_timing(sn_ctx *c) {
 
 static int check_ready(sn_ctx *c, bool token) {
     if (!c) return SN_E_INVALID;
+    if (c->state == ST_FAILED) return fail(c, SN_E_STATE, "context unusable after a failed re-plan");
     if (c->state != ST_PLANNED) return fail(c, SN_E_STATE, "inference before sn_plan");
     if (c->host_only) return fail(c, SN_E_UNSUPPORTED, "host-only context cannot run");
     if (c->token != token)
@@ -1045,6 +1087,88 @@ extern "C" int sn_reset(sn_ctx *c) {
     if (!c) return SN_E_INVALID;
     if (c->state != ST_PLANNED) return fail(c, SN_E_STATE, "sn_reset before sn_plan");
     c->pos = 0;
+    return SN_OK;
+}
+
+// Re-plan in place.  Sec. 6 forms blocks from the layers extracted once at
+// registration, so that a new budget only changes which layers each block
+// references; here the layers' device-layout tensors are gathered back from
+// the pinned image, cut into the new partition and written to a new image.
+// Activations, the KV cache and the token position are kept.
+extern "C" int sn_replan(sn_ctx *c, size_t budget_bytes) {
+    if (!c) return SN_E_INVALID;
+    if (c->state != ST_PLANNED) return fail(c, SN_E_STATE, "sn_replan before sn_plan");
+    const int64_t B = budget_bytes ? (int64_t)budget_bytes : c->budget;
+    if (B < kAlign) return fail(c, SN_E_INVALID, "budget must be at least 256 bytes");
+    const int64_t split = c->split_explicit ? c->split_budget : B;
+    if (!c->host_only) {
+        if (c->copier.joinable()) wait_copier_idle(c);
+        if (c->have_prev) HIP_TRY(c, hipEventSynchronize(c->ev_end));
+        for (hipStream_t st : {c->comp_s, c->copy_s, c->copy_s2})
+            if (st) HIP_TRY(c, hipStreamSynchronize(st));
+    }
+    // the new partition first: on failure the context stays as it was
+    PlanResult next;
+    std::string err;
+    int rc = plan_slabs(c->layers, c->n_blocks, split, B, c->max_slab, c->partition, c->cost, next, err);
+    if (!rc) rc = place_slabs(next, B, err);
+    if (rc) return fail(c, rc, err);
+    uint8_t *arena = c->arena, *image = nullptr, *image_dev = nullptr;
+    const size_t img = (size_t)std::max<int64_t>(next.image_bytes, 1);
+    if (c->host_only) {
+        image = (uint8_t *)malloc(img);
+        if (!image) return fail(c, SN_E_NOMEM, "host image allocation failed");
+    } else {
+        if (B > c->arena_bytes) HIP_TRY(c, hipMalloc((void **)&arena, (size_t)B));
+        hipError_t e = hipHostMalloc((void **)&image, img, hipHostMallocMapped);
+        if (e == hipSuccess) e = hipHostGetDevicePointer((void **)&image_dev, image, 0);
+        if (e != hipSuccess) {
+            if (image) hipHostFree(image);
+            if (arena != c->arena) hipFree(arena);
+            return fail(c, SN_E_NOMEM, std::string("re-plan allocation: ") + hipGetErrorString(e));
+        }
+    }
+    // device-layout tensors of every layer, from the current image
+    for (const Slab &sl : c->plan.slabs)
+        for (int pi : sl.pieces) {
+            const Piece &p = c->plan.pieces[pi];
+            Layer &Ly = c->layers[p.layer];
+            if (p.w_bytes) {
+                Ly.w_dev.resize((size_t)(Ly.units * Ly.w_unit_bytes / 2));
+                memcpy((uint8_t *)Ly.w_dev.data() + p.u0 * Ly.w_unit_bytes, c->image + sl.image_off + p.w_off,
+                       (size_t)p.w_bytes);
+            }
+            if (p.b_bytes) {
+                Ly.b_dev.resize((size_t)(Ly.units * Ly.b_unit_bytes / 2));
+                memcpy((uint8_t *)Ly.b_dev.data() + p.u0 * Ly.b_unit_bytes, c->image + sl.image_off + p.b_off,
+                       (size_t)p.b_bytes);
+            }
+        }
+    write_image(c->layers, next, image);
+    for (Layer &Ly : c->layers) {
+        std::vector<uint16_t>().swap(Ly.w_dev);
+        std::vector<uint16_t>().swap(Ly.b_dev);
+    }
+    if (c->host_only) {
+        free(c->image);
+    } else {
+        release_plan_resources(c);
+        hipHostFree(c->image);
+        if (arena != c->arena) {
+            hipFree(c->arena);
+            c->arena_bytes = B;
+        }
+    }
+    c->arena = arena;
+    c->image = image;
+    c->image_dev = image_dev;
+    c->plan = next;
+    c->budget = B;
+    c->split_budget = split;
+    if (!c->host_only && (rc = setup_plan_resources(c))) {
+        c->state = ST_FAILED;
+        return rc;
+    }
     return SN_OK;
 }
 
@@ -1331,6 +1455,68 @@ static int calibrate_impl(sn_ctx *c, int reps, CostModel &m) {
         }
     }
     return rc;
+}
+
+
+// Measured choice among the partitions (the paper prunes its lookup table of
+// predicted latencies by the budget and takes the least; here the
+// prediction proposes partition 2 and measurement decides among it and
+// partitions 0 and 1): the delay model is calibrated on the current plan,
+// then each partition is planned in place and timed over 8 inferences issued
+// back to back, and the fastest is kept.
+static int time_back_to_back(sn_ctx *c, double &t) {
+    const int K = 8;
+    int rc = SN_OK;
+    for (int w = 0; w < 2 && !rc; ++w) rc = calib_enqueue(c);
+    if (!rc) HIP_TRY(c, hipStreamSynchronize(c->comp_s));
+    if (!rc) HIP_TRY(c, hipEventRecord(c->t_start, c->comp_s));
+    for (int k = 0; k < K && !rc; ++k) rc = calib_enqueue(c);
+    if (rc) return rc;
+    HIP_TRY(c, hipEventRecord(c->t_ex0[0], c->comp_s));
+    HIP_TRY(c, hipStreamSynchronize(c->comp_s));
+    if ((rc = check_copier(c))) return rc;
+    float ms = 0;
+    HIP_TRY(c, hipEventElapsedTime(&ms, c->t_start, c->t_ex0[0]));
+    t = ms * 1e-3 / K;
+    return SN_OK;
+}
+
+extern "C" int sn_tune(sn_ctx *c, int reps, double *times_s) {
+    int rc = check_ready(c, c ? c->token : false);
+    if (rc) return rc;
+    if (reps < 1 || reps > 64) return fail(c, SN_E_INVALID, "reps must be in [1, 64]");
+    if (c->token && c->pos >= c->max_seq) return fail(c, SN_E_INVALID, "KV cache full (max_seq reached)");
+    if (times_s)
+        for (int p = 0; p < 3; ++p) times_s[p] = 0;
+    if (c->plan.resident) return SN_OK;
+    HIP_TRY(c, ensure_stream(&c->comp_s));
+    CostModel m = c->cost;
+    if ((rc = calibrate_impl(c, reps, m))) return rc;
+    c->cost = m;
+    const int orig = c->partition;
+    int best = -1;
+    double best_t = 0;
+    for (int p = 0; p < 3; ++p) {
+        c->partition = p;
+        rc = sn_replan(c, 0);
+        if (rc == SN_E_INFEASIBLE) continue;
+        if (rc) return rc;
+        double t = 0;
+        for (int r = 0; r < std::max(1, reps / 2) && !rc; ++r) {
+            double x = 0;
+            rc = time_back_to_back(c, x);
+            t = r ? std::min(t, x) : x;
+        }
+        if (rc) return rc;
+        if (times_s) times_s[p] = t;
+        if (best < 0 || t < best_t) {
+            best = p;
+            best_t = t;
+        }
+    }
+    c->partition = best >= 0 ? best : orig;
+    if (c->partition != 2) return sn_replan(c, 0);
+    return SN_OK;
 }
 
 extern "C" int sn_calibrate(sn_ctx *c, int reps) {

@@ -34,7 +34,8 @@ OPT_SYNC = 9
 EXPORTS = ["sn_create", "sn_create_ex", "sn_add_block", "sn_plan", "sn_set_option", "sn_infer",
            "sn_infer_dev", "sn_infer_tokens", "sn_reset", "sn_get_stats", "sn_get_slab",
            "sn_get_piece", "sn_get_image", "sn_kernel_name", "sn_last_error", "sn_destroy",
-           "sn_set_cost_model", "sn_get_cost_model", "sn_calibrate", "sn_predict"]
+           "sn_set_cost_model", "sn_get_cost_model", "sn_calibrate", "sn_predict", "sn_replan",
+           "sn_tune"]
 COST_KEYS = ("alpha", "beta", "gamma", "kappa", "gate", "wake", "slab_ex")
 
 
@@ -107,6 +108,8 @@ def load_library(path=LIB_PATH):
         "sn_set_cost_model": (I, [P, C.POINTER(SnCostModel)]),
         "sn_get_cost_model": (I, [P, C.POINTER(SnCostModel), P, I]),
         "sn_calibrate": (I, [P, I]),
+        "sn_replan": (I, [P, S]),
+        "sn_tune": (I, [P, I, C.POINTER(C.c_double)]),
         "sn_predict": (I, [P, C.POINTER(C.c_double), C.POINTER(C.c_double)]),
         "sn_last_error": (C.c_char_p, [P]), "sn_destroy": (None, [P]),
     }
@@ -255,6 +258,21 @@ class SwapNet:
         out = {k: getattr(m, k) for k in COST_KEYS}
         out["layer_ex"] = ex[:n].copy()
         return out
+
+    def replan(self, budget=0):
+        """Re-plan in place for ``budget`` bytes (0: keep) and the current
+        options."""
+        r = self._check(self.lib.sn_replan(self.ctx, int(budget)))
+        if budget:
+            self.budget = int(budget)
+        return r
+
+    def tune(self, reps=3):
+        """Measure partitions 0, 1 and 2 and keep the fastest; returns the
+        measured seconds per inference of each (0: infeasible)."""
+        t = (C.c_double * 3)()
+        self._check(self.lib.sn_tune(self.ctx, int(reps), t))
+        return list(t)
 
     def calibrate(self, reps=3):
         return self._check(self.lib.sn_calibrate(self.ctx, int(reps)))

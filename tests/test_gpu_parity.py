@@ -291,6 +291,55 @@ def test_decoder_calibration_keeps_generation():
     assert np.array_equal(runs[0].view(np.uint32), runs[1].view(np.uint32))
 
 
+def test_replan_in_place_keeps_results():
+    # one context re-planned for a smaller budget, for a budget above its
+    # arena (resident: a new arena) and for the balanced partition computes
+    # the same bits every time
+    net, wts, x, ref = net_case("resnet50", res=96)
+    B = net.weight_bytes()
+    with S.build_engine(net, wts, budget=int(B / 2.32)) as eng:
+        y0 = eng.infer(x)
+        for budget, partition, resident in ((int(B / 5.81), 0, 0), (2 * B, 0, 1), (int(B / 3), 1, 0)):
+            eng.set_option(S.OPT_PARTITION, partition)
+            eng.replan(budget)
+            assert eng.stats()["resident"] == resident
+            y = eng.infer(x)
+            assert np.array_equal(y.view(np.uint16), y0.view(np.uint16)), (budget, partition)
+    assert rel_err(y0, ref) <= TOL
+
+
+def test_tune_keeps_the_fastest_partition():
+    net, wts, x, _ = net_case("fcn_resnet101", res=128)
+    with S.build_engine(net, wts, budget=int(net.weight_bytes() / 4)) as eng:
+        y0 = eng.infer(x)
+        t = eng.tune(2)
+        assert all(v >= 0 for v in t) and sum(1 for v in t if v > 0) >= 2, t
+        y = eng.infer(x)
+        assert np.array_equal(y.view(np.uint16), y0.view(np.uint16))
+
+
+def test_decoder_replan_mid_generation():
+    # a token network re-planned between tokens keeps its KV cache and
+    # position: the generation continues as if nothing happened
+    net = small_decoder()
+    wts = W.make_weights(net)
+    prompt = W.make_input(net)
+    lb = sum(l.weight_bytes() for l in net.layers[1:8])
+    runs = []
+    for replan in (False, True):
+        with S.build_engine(net, wts, budget=2 * lb) as eng:
+            rows = [eng.infer_tokens(prompt)]
+            for k in range(5):
+                if replan and k == 2:
+                    eng.replan(3 * lb)
+                if replan and k == 4:
+                    eng.set_option(S.OPT_PARTITION, 1)
+                    eng.replan(2 * lb)
+                rows.append(eng.infer_tokens(np.array([int(np.argmax(rows[-1]))], np.int32)))
+            runs.append(np.stack(rows))
+    assert np.array_equal(runs[0].view(np.uint32), runs[1].view(np.uint32))
+
+
 def test_decoder_long_context_split_attention():
     # 200-token prompt: single-token steps attend over 200+ cached positions,
     # which the attention kernel splits over several blocks (per-chunk

@@ -175,3 +175,46 @@ def test_cost_model_api_round_trip_and_errors():
         eng.calibrate(3)
     assert e.value.code == S.SN_E_UNSUPPORTED
     eng.close()
+
+
+@pytest.mark.parametrize("name", ["resnet50", "fcn_resnet101"])
+def test_replan_in_place_equals_a_fresh_plan(name):
+    # re-forming the slabs from the registered layers (no re-registration)
+    # gives the very image a fresh plan at that budget / partition gives
+    net, wts = weights_of(name)
+    B1, B2 = int(net.weight_bytes() / 2.32), int(net.weight_bytes() / 5.81)
+    eng = S.build_engine(net, wts, budget=B1, host_only=True)
+    img1 = eng.image()
+    eng.replan(B2)
+    with S.build_engine(net, wts, budget=B2, host_only=True) as fresh:
+        assert np.array_equal(eng.image(), fresh.image())
+        assert eng.slabs() == fresh.slabs()
+    eng.set_option(S.OPT_PARTITION, 1)
+    eng.replan()
+    with S.build_engine(net, wts, budget=B2, host_only=True, partition=1) as fresh:
+        assert np.array_equal(eng.image(), fresh.image())
+    eng.set_option(S.OPT_PARTITION, 0)
+    eng.replan(B1)
+    assert np.array_equal(eng.image(), img1)
+    assert eng.stats()["budget_bytes"] == B1
+    eng.close()
+
+
+def test_replan_errors_leave_the_context_unchanged():
+    net, wts = weights_of("resnet50")
+    eng = S.SwapNet(int(net.weight_bytes() / 3), host_only=True)
+    with pytest.raises(S.SwapNetError) as e:
+        eng.replan(1 << 20)
+    assert e.value.code == S.SN_E_STATE
+    for a, b in net.blocks:
+        eng.add_block(*S.block_payload(net, wts, a, b))
+    eng.plan()
+    img, sl = eng.image(), eng.slabs()
+    with pytest.raises(S.SwapNetError) as e:
+        eng.replan(4096)            # no layer fits half of it
+    assert e.value.code == S.SN_E_INFEASIBLE
+    with pytest.raises(S.SwapNetError) as e:
+        eng.replan(100)
+    assert e.value.code == S.SN_E_INVALID
+    assert np.array_equal(eng.image(), img) and eng.slabs() == sl
+    eng.close()
