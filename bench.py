@@ -64,6 +64,8 @@ def parse():
                     help="DMA queues used by the copy thread (consecutive slabs alternate)")
     ap.add_argument("--swapin-blocks", type=int, default=None,
                     help="workgroups of the copy kernel (--swapin 0)")
+    ap.add_argument("--ablation", action="store_true",
+                    help="also time the naive swapping modes (SN_OPT_NAIVE), untimed in `value`")
     ap.add_argument("--pmc-calibration", action="store_true",
                     help="also run one 256 MiB device-to-device copy (counter calibration)")
     return ap.parse_args()
@@ -458,6 +460,19 @@ def main():
     torch.cuda.synchronize()
     bitwise = bool(torch.equal(yd.view(torch.int16), yr.view(torch.int16)))
 
+    ablation = None
+    if a.ablation:
+        # the redundant memory operations of plain swapping, put back one at
+        # a time (sequential = swap-in then compute, slab after slab)
+        ablation = {}
+        for name, flags in (("sequential", 1), ("sequential + hipMalloc/hipFree per swap", 3),
+                            ("sequential + pageable source", 5),
+                            ("sequential + copy-based assembly", 9), ("all three", 15)):
+            log("ablation: %s" % name)
+            eng_sw.set_option(S.OPT_NAIVE, flags)
+            ablation[name] = round(timed_loop(torch, eng_sw, xd, yd, 10, 2)[0], 4)
+        eng_sw.set_option(S.OPT_NAIVE, 0)
+
     streamed = st["streamed_bytes"]
     h2d = streamed / (sw_ms * 1e-3) / 1e9
     log("timing the swap-in copies alone")
@@ -538,6 +553,7 @@ def main():
                         "calibrated_on": "this plan" if cm is None else "workload-block plan"},
         "kernels": {k: {"launches": v[0], "ms": round(v[1], 4)} for k, v in groups.items()},
         "swapped_equals_resident_bitwise": bitwise,
+        "ablation_ms": ablation,
         "partition_candidates_ms": None if tuned is None else
             {n: round(t * 1e3, 4) if t else None for n, t in zip(PARTITIONS, tuned)},
         "activation_bytes": st["activation_bytes"],

@@ -220,6 +220,12 @@ enum sn_option {
                                    memory (hipStreamWriteValue64 /
                                    hipStreamWaitValue64) for both.  May be
                                    set after plan, between inferences         */
+    SN_OPT_NAIVE = 10,          /* measurement only: flags of sn_naive_flag;
+                                   0 (default) = the engine as described.  Any
+                                   other value runs a swapped plan slab after
+                                   slab on the compute stream (no overlap, no
+                                   graphs, no copy thread).  May be set after
+                                   plan, between inferences                   */
     SN_OPT_GRAPH = 4            /* 1 (default): the kernels of each slab of an
                                    image network are captured once per
                                    (input, output) buffer pair into one HIP
@@ -229,6 +235,21 @@ enum sn_option {
                                    SN_OPT_TIMING is on, nor for token nets    */
 };
 int sn_set_option(sn_ctx *ctx, int option, int64_t value);
+
+/* SN_OPT_NAIVE flags: the redundant memory operations the paper removes
+ * (Sec. 4.2: a swap-in that allocates and copies through a staging path;
+ * Sec. 5.2: assembly that copies parameters into a model), put back one by
+ * one to measure what each costs on this hardware. */
+enum sn_naive_flag {
+    SN_NAIVE_SEQUENTIAL = 1,    /* swap-in then compute, slab after slab      */
+    SN_NAIVE_ALLOC = 2,         /* hipMalloc per swap-in, hipFree after the
+                                   slab's compute (instead of the arena)      */
+    SN_NAIVE_PAGEABLE = 4,      /* copy from pageable host memory (a malloc'd
+                                   copy of the image) with hipMemcpy          */
+    SN_NAIVE_COPY_ASSEMBLY = 8  /* copy every parameter tensor, one
+                                   hipMemcpyAsync each, into a second device
+                                   allocation and bind the kernels to that    */
+};
 
 /* Delay model of a swapped run (Sec. 5: input, execution and output delays
  * of a block, each linear in the block's bytes, parameter depth or FLOPs,

@@ -97,6 +97,8 @@ struct sn_ctx {
     int64_t act_bytes = 0;
     uint8_t *kv = nullptr;
     int partition = 0;                 // SN_OPT_PARTITION
+    int naive = 0;                     // SN_OPT_NAIVE flags
+    uint8_t *image_pageable = nullptr; // pageable copy of the image (SN_NAIVE_PAGEABLE)
     CostModel cost;                    // delay model (sn_set_cost_model / sn_calibrate)
     int64_t kv_bytes = 0;
     int64_t attn_ws_bytes = 0;
@@ -282,6 +284,11 @@ extern "C" int sn_set_option(sn_ctx *c, int option, int64_t value) {
         if ((int)value != c->sync) drop_graphs(c);   // the graphs hold the signal kernels
         c->sync = (int)value;
         return SN_OK;
+    case SN_OPT_NAIVE:
+        if (value < 0 || value > 15) return fail(c, SN_E_INVALID, "naive flags must be in [0, 15]");
+        if (c->state == ST_PLANNED && c->have_prev) wait_copier_idle(c);
+        c->naive = (int)value;
+        return SN_OK;
     case SN_OPT_PARTITION:
         if (value < 0 || value > 2) return fail(c, SN_E_INVALID, "partition must be 0, 1 or 2");
         c->partition = (int)value;
@@ -306,6 +313,16 @@ static void choose_layer_kernels(sn_ctx *c) {
 
 static uint8_t *slot_ptr(sn_ctx *c, int id) { return c->act + c->slots[id].off; }
 
+// Binding (assembly by reference): the parameter pointers of slab i's
+// pieces, for the slab's bytes at `base`.
+static void bind_slab(sn_ctx *c, int i, const uint8_t *base) {
+    for (int pi : c->plan.slabs[i].pieces) {
+        const Piece &p = c->plan.pieces[pi];
+        c->piece_w[pi] = p.w_bytes ? base + p.w_off : nullptr;
+        c->piece_b[pi] = p.b_bytes ? base + p.b_off : nullptr;
+    }
+}
+
 // Everything that depends on the slab partition: the binding table
 // (assembly by reference: parameter pointers into the arena), per-slab and
 // per-piece events, the copy thread and its counters, and for a resident
@@ -315,12 +332,7 @@ static int setup_plan_resources(sn_ctx *c) {
     const int np = (int)c->plan.pieces.size();
     c->piece_w.assign(np, nullptr);
     c->piece_b.assign(np, nullptr);
-    for (const Slab &s : c->plan.slabs)
-        for (int pi : s.pieces) {
-            const Piece &p = c->plan.pieces[pi];
-            if (p.w_bytes) c->piece_w[pi] = c->arena + s.arena_off + p.w_off;
-            if (p.b_bytes) c->piece_b[pi] = c->arena + s.arena_off + p.b_off;
-        }
+    for (int i = 0; i < (int)c->plan.slabs.size(); ++i) bind_slab(c, i, c->arena + c->plan.slabs[i].arena_off);
 
     const int ns = (int)c->plan.slabs.size();
     c->loaded.assign(ns, nullptr);
@@ -798,8 +810,69 @@ static hipError_t signal_done(sn_ctx *c, int i, uint64_t seq, hipStream_t cs) {
     return launch_signal(c->sig_dev + i, cs);
 }
 
+
+// Naive swapping, for measurement only (SN_OPT_NAIVE): one slab after the
+// other on the compute stream, no overlap and no graphs, with optionally the
+// redundant memory operations the paper removes (Sec. 4 and 5): a device
+// allocation per swap-in freed after the slab's compute, a pageable source
+// (the runtime stages it through its own pinned buffer), and assembly by
+// copying every parameter tensor into separately allocated model buffers.
+template <typename Pre, typename Post>
+static int run_naive(sn_ctx *c, int n_tok, hipStream_t cs, Pre pre, Post post) {
+    const int ns = (int)c->plan.slabs.size();
+    if (c->copier.joinable()) wait_copier_idle(c);
+    ++c->seq;
+    c->prev_threaded = false;
+    if ((c->naive & SN_NAIVE_PAGEABLE) && !c->image_pageable) {
+        c->image_pageable = (uint8_t *)malloc((size_t)std::max<int64_t>(c->plan.image_bytes, 1));
+        if (!c->image_pageable) return fail(c, SN_E_NOMEM, "pageable image allocation failed");
+        memcpy(c->image_pageable, c->image, (size_t)c->plan.image_bytes);
+    }
+    int rc = SN_OK;
+    for (int i = 0; i < ns && !rc; ++i) {
+        const Slab &s = c->plan.slabs[i];
+        uint8_t *buf = c->arena + s.arena_off, *params = nullptr;
+        if (s.bytes && (c->naive & SN_NAIVE_ALLOC)) HIP_TRY(c, hipMalloc((void **)&buf, (size_t)s.bytes));
+        if (s.bytes && (c->naive & SN_NAIVE_PAGEABLE)) {
+            HIP_TRY(c, hipStreamSynchronize(cs));
+            HIP_TRY(c, hipMemcpy(buf, c->image_pageable + s.image_off, (size_t)s.bytes, hipMemcpyHostToDevice));
+        } else if (s.bytes) {
+            HIP_TRY(c, hipMemcpyAsync(buf, c->image + s.image_off, (size_t)s.bytes, hipMemcpyHostToDevice, cs));
+        }
+        const uint8_t *base = buf;
+        if (s.bytes && (c->naive & SN_NAIVE_COPY_ASSEMBLY)) {
+            HIP_TRY(c, hipMalloc((void **)&params, (size_t)s.bytes));
+            for (int pi : s.pieces) {
+                const Piece &p = c->plan.pieces[pi];
+                if (p.w_bytes)
+                    HIP_TRY(c, hipMemcpyAsync(params + p.w_off, buf + p.w_off, (size_t)p.w_bytes,
+                                              hipMemcpyDeviceToDevice, cs));
+                if (p.b_bytes)
+                    HIP_TRY(c, hipMemcpyAsync(params + p.b_off, buf + p.b_off, (size_t)p.b_bytes,
+                                              hipMemcpyDeviceToDevice, cs));
+            }
+            base = params;
+        }
+        bind_slab(c, i, base);
+        if (i == 0) rc = pre(cs);
+        if (!rc) rc = slab_kernels(c, i, n_tok, cs);
+        if (!rc && i == ns - 1) rc = post(cs);
+        bind_slab(c, i, c->arena + s.arena_off);
+        if (buf != c->arena + s.arena_off || params) {
+            // freeing device memory waits for the work that uses it
+            hipError_t e = hipStreamSynchronize(cs);
+            if (buf != c->arena + s.arena_off) hipFree(buf);
+            if (params) hipFree(params);
+            if (!rc && e != hipSuccess) rc = fail(c, SN_E_HIP, hipGetErrorString(e));
+        }
+    }
+    if (!rc) c->complete_seq.store(c->seq);
+    return rc;
+}
+
 template <typename Pre, typename Post>
 static int run_slabs(sn_ctx *c, int n_tok, hipStream_t cs, Pre pre, Post post, bool graphs) {
+    if (c->naive && !c->plan.resident) return run_naive(c, n_tok, cs, pre, post);
     const int ns = (int)c->plan.slabs.size();
     const bool swap = !c->plan.resident;
     const bool threaded = swap && c->swapin == 2;
@@ -1002,7 +1075,7 @@ static int capture_graphs(sn_ctx *c, const void *d_in, void *d_out) {
 static int infer_dev_impl(sn_ctx *c, const void *d_in, void *d_out, hipStream_t cs) {
     // inferences are serialised: activations and arena are shared
     if (c->have_prev) HIP_TRY(c, hipStreamWaitEvent(cs, c->ev_end, 0));
-    const bool graphs = c->use_graph && !c->timing;
+    const bool graphs = c->use_graph && !c->timing && !(c->naive && !c->plan.resident);
     int rc;
     if (graphs && (c->graphs.empty() || c->g_in != d_in || c->g_out != d_out))
         if ((rc = capture_graphs(c, d_in, d_out))) return rc;
@@ -1162,6 +1235,8 @@ extern "C" int sn_replan(sn_ctx *c, size_t budget_bytes) {
     c->arena = arena;
     c->image = image;
     c->image_dev = image_dev;
+    free(c->image_pageable);
+    c->image_pageable = nullptr;
     c->plan = next;
     c->budget = B;
     c->split_budget = split;
@@ -1641,5 +1716,6 @@ extern "C" void sn_destroy(sn_ctx *c) {
     } else {
         free(c->image);
     }
+    free(c->image_pageable);
     delete c;
 }

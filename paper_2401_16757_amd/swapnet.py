@@ -30,6 +30,8 @@ OPT_SPLIT_BUDGET, OPT_TIMING, OPT_MAX_SLAB, OPT_GRAPH, OPT_SWAPIN, OPT_SWAPIN_BL
 OPT_COPY_STREAMS = 7
 OPT_PARTITION = 8
 OPT_SYNC = 9
+OPT_NAIVE = 10
+NAIVE_SEQUENTIAL, NAIVE_ALLOC, NAIVE_PAGEABLE, NAIVE_COPY_ASSEMBLY = 1, 2, 4, 8
 
 EXPORTS = ["sn_create", "sn_create_ex", "sn_add_block", "sn_plan", "sn_set_option", "sn_infer",
            "sn_infer_dev", "sn_infer_tokens", "sn_reset", "sn_get_stats", "sn_get_slab",

@@ -308,6 +308,23 @@ def test_replan_in_place_keeps_results():
     assert rel_err(y0, ref) <= TOL
 
 
+@pytest.mark.parametrize("flags", [1, 3, 5, 9, 15])
+def test_naive_swapping_modes_compute_the_same(flags):
+    # the measurement-only naive modes (sequential, per-swap allocation,
+    # pageable source, copy-based assembly) run the same kernels on the same
+    # bytes: bit-identical to the engine's own path
+    net, wts, x, _ = net_case("resnet50", res=96)
+    with S.build_engine(net, wts, budget=int(net.weight_bytes() / 5.81)) as eng:
+        y0 = eng.infer(x)
+        eng.set_option(S.OPT_NAIVE, flags)
+        y1 = eng.infer(x)
+        y2 = eng.infer(x)
+        eng.set_option(S.OPT_NAIVE, 0)
+        y3 = eng.infer(x)
+    for y in (y1, y2, y3):
+        assert np.array_equal(y.view(np.uint16), y0.view(np.uint16)), flags
+
+
 def test_tune_keeps_the_fastest_partition():
     net, wts, x, _ = net_case("fcn_resnet101", res=128)
     with S.build_engine(net, wts, budget=int(net.weight_bytes() / 4)) as eng:
