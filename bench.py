@@ -560,6 +560,15 @@ def main():
         "hip_graph": not a.no_graph,
         "swapin_mode": {0: "copy kernel", 1: "SDMA, calling thread", 2: "SDMA, copy thread"}[a.swapin],
     }
+    # runtime adaptation (Sec. 6): re-plan in place for half the budget and
+    # back, with the workload's blocks (host wall time of each sn_replan)
+    eng_sw.set_option(S.OPT_PARTITION, 0)
+    t0 = time.perf_counter()
+    eng_sw.replan(budget // 2)
+    t1 = time.perf_counter()
+    eng_sw.replan(budget)
+    t2 = time.perf_counter()
+    out["replan_ms"] = {"to_half_budget": round((t1 - t0) * 1e3, 2), "back": round((t2 - t1) * 1e3, 2)}
     if not a.no_cpu_baseline:
         log("CPU oracle baseline (~%.0f s)" % a.cpu_seconds)
         out["cpu_baseline"] = cpu_baseline(net, wts, x, a.cpu_seconds)

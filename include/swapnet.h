@@ -163,6 +163,17 @@ int sn_plan(sn_ctx *ctx);
  * the introspection calls remain). */
 int sn_replan(sn_ctx *ctx, size_t budget_bytes);
 
+/* Budgets of n models sharing `total` bytes of device memory (Sec. 6,
+ * Eq. 1).  If the demands need[i] (bytes) fit, out[i] = need[i].  Otherwise
+ *   out[i] = need[i] / sum(need) * (1 - 1/n) * total
+ *          + PS[i] / sum(PS) * (1/n) * total,   PS[i] = urgency[i] *
+ *            latency_s[i] / need[i]
+ * (equal shares of the second part if every PS is 0), each rounded down to
+ * a multiple of 256 bytes.  Host only; no context.  Errors: SN_E_INVALID
+ * (n <= 0, NULL, need <= 0, negative or non-finite latency or urgency). */
+int sn_split_budget(int n, const int64_t *need, const double *latency_s, const double *urgency,
+                    int64_t total, int64_t *out);
+
 /* Options (set before sn_plan unless noted; SN_OPT_SPLIT_BUDGET,
  * SN_OPT_MAX_SLAB and SN_OPT_PARTITION may also be set later and take
  * effect at the next sn_replan). */

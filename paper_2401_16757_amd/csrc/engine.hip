@@ -1248,6 +1248,37 @@ extern "C" int sn_replan(sn_ctx *c, size_t budget_bytes) {
 }
 
 // ---------------------------------------------------------------------------
+// Several models in one memory budget (Sec. 6, Eq. 1): each model gets its
+// share of (1 - 1/n) of the memory in proportion to its demand, and of the
+// remaining 1/n in proportion to its performance score PS = u * latency /
+// memory (urgency times latency per byte).  Host only.
+// ---------------------------------------------------------------------------
+extern "C" int sn_split_budget(int n, const int64_t *need, const double *latency_s,
+                               const double *urgency, int64_t total, int64_t *out) {
+    if (n <= 0 || !need || !latency_s || !urgency || !out || total < 0) return SN_E_INVALID;
+    double sum_need = 0, sum_ps = 0;
+    std::vector<double> ps(n);
+    for (int i = 0; i < n; ++i) {
+        if (need[i] <= 0 || !std::isfinite(latency_s[i]) || latency_s[i] < 0 || !std::isfinite(urgency[i]) ||
+            urgency[i] < 0)
+            return SN_E_INVALID;
+        sum_need += (double)need[i];
+        ps[i] = urgency[i] * latency_s[i] / (double)need[i];
+        sum_ps += ps[i];
+    }
+    if (sum_need <= (double)total) {   // everything fits: each model gets its demand
+        for (int i = 0; i < n; ++i) out[i] = need[i];
+        return SN_OK;
+    }
+    for (int i = 0; i < n; ++i) {
+        const double by_need = (double)need[i] / sum_need * (1.0 - 1.0 / n) * (double)total;
+        const double by_score = (sum_ps > 0 ? ps[i] / sum_ps : 1.0 / n) / n * (double)total;
+        out[i] = (int64_t)(by_need + by_score) / kAlign * kAlign;
+    }
+    return SN_OK;
+}
+
+// ---------------------------------------------------------------------------
 // Delay model (Sec. 5): the context's coefficients, their measurement on the
 // device, and the predicted time of the plan.
 // ---------------------------------------------------------------------------

@@ -37,7 +37,7 @@ EXPORTS = ["sn_create", "sn_create_ex", "sn_add_block", "sn_plan", "sn_set_optio
            "sn_infer_dev", "sn_infer_tokens", "sn_reset", "sn_get_stats", "sn_get_slab",
            "sn_get_piece", "sn_get_image", "sn_kernel_name", "sn_last_error", "sn_destroy",
            "sn_set_cost_model", "sn_get_cost_model", "sn_calibrate", "sn_predict", "sn_replan",
-           "sn_tune"]
+           "sn_tune", "sn_split_budget"]
 COST_KEYS = ("alpha", "beta", "gamma", "kappa", "gate", "wake", "slab_ex")
 
 
@@ -112,6 +112,8 @@ def load_library(path=LIB_PATH):
         "sn_calibrate": (I, [P, I]),
         "sn_replan": (I, [P, S]),
         "sn_tune": (I, [P, I, C.POINTER(C.c_double)]),
+        "sn_split_budget": (I, [I, C.POINTER(C.c_int64), C.POINTER(C.c_double),
+                                C.POINTER(C.c_double), C.c_int64, C.POINTER(C.c_int64)]),
         "sn_predict": (I, [P, C.POINTER(C.c_double), C.POINTER(C.c_double)]),
         "sn_last_error": (C.c_char_p, [P]), "sn_destroy": (None, [P]),
     }
@@ -125,6 +127,20 @@ def load_library(path=LIB_PATH):
 
 def kernel_name(kernel_id):
     return load_library().sn_kernel_name(int(kernel_id)).decode()
+
+
+def split_budget(need, latency_s, urgency, total):
+    """Budgets of several models sharing ``total`` bytes (sn_split_budget)."""
+    lib = load_library()
+    n = len(need)
+    a_need = (C.c_int64 * n)(*[int(v) for v in need])
+    a_lat = (C.c_double * n)(*[float(v) for v in latency_s])
+    a_urg = (C.c_double * n)(*[float(v) for v in urgency])
+    out = (C.c_int64 * n)()
+    rc = lib.sn_split_budget(n, a_need, a_lat, a_urg, int(total), out)
+    if rc != SN_OK:
+        raise SwapNetError(rc, "invalid arguments to sn_split_budget")
+    return list(out)
 
 
 class SwapNetError(RuntimeError):

@@ -335,6 +335,30 @@ def test_tune_keeps_the_fastest_partition():
         assert np.array_equal(y.view(np.uint16), y0.view(np.uint16))
 
 
+def test_two_models_share_a_budget_and_adapt():
+    # Eq. 1 splits one budget between two models; when the total shrinks,
+    # both are re-planned in place and compute the same bits
+    cases = [net_case("resnet50", res=96), net_case("fcn_resnet101", res=128)]
+    need = [c[0].weight_bytes() for c in cases]
+    engines, outs = [], []
+    budgets = S.split_budget(need, [1e-3, 2e-3], [1.0, 1.0], sum(need) // 2)
+    for (net, wts, x, ref), b in zip(cases, budgets):
+        eng = S.build_engine(net, wts, budget=b)
+        assert not eng.stats()["resident"]
+        y = eng.infer(x)
+        assert rel_err(y, ref) <= TOL
+        engines.append(eng)
+        outs.append(y)
+    smaller = S.split_budget(need, [1e-3, 2e-3], [1.0, 1.0], int(sum(need) * 0.35))
+    assert all(a < b for a, b in zip(smaller, budgets))
+    for eng, b, (net, wts, x, _), y0 in zip(engines, smaller, cases, outs):
+        eng.replan(b)
+        assert eng.stats()["budget_bytes"] == b
+        y = eng.infer(x)
+        assert np.array_equal(y.view(np.uint16), y0.view(np.uint16))
+        eng.close()
+
+
 def test_decoder_replan_mid_generation():
     # a token network re-planned between tokens keeps its KV cache and
     # position: the generation continues as if nothing happened

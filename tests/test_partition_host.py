@@ -218,3 +218,29 @@ def test_replan_errors_leave_the_context_unchanged():
     assert e.value.code == S.SN_E_INVALID
     assert np.array_equal(eng.image(), img) and eng.slabs() == sl
     eng.close()
+
+
+def test_split_budget_follows_eq1():
+    GB = 1 << 30
+    # the paper's example: 1.5 GB of demand in 1 GB; with equal scores the
+    # first term gives each model 2/3 of its demand times (1 - 1/n), the
+    # reserved 1/n is shared equally
+    out = S.split_budget([GB // 2, GB], [1.0, 2.0], [1.0, 1.0], GB)
+    # PS = latency / memory: 1/(GB/2) and 2/GB are equal
+    want = [(1 / 3) * 0.5 * GB + 0.5 * 0.5 * GB, (2 / 3) * 0.5 * GB + 0.5 * 0.5 * GB]
+    assert all(abs(o - w) < 256 for o, w in zip(out, want)), (out, want)
+    assert all(o % 256 == 0 for o in out) and sum(out) <= GB
+    # scores proportional to demand: both terms proportional, shares = demand share
+    need = [3 * GB, 5 * GB, 8 * GB]
+    lat = [n * n / GB for n in need]          # PS = latency / memory = need / GB
+    out = S.split_budget(need, lat, [1, 1, 1], 4 * GB)
+    for o, n in zip(out, need):
+        assert abs(o - n / sum(need) * 4 * GB) < 256
+    # one model: all of it; demands that fit: the demands
+    assert S.split_budget([5 * GB], [0.1], [1.0], GB) == [GB]
+    assert S.split_budget([GB, GB], [1, 1], [1, 1], 3 * GB) == [GB, GB]
+    # urgency moves the reserved share only
+    a = S.split_budget([GB, GB], [1, 1], [1, 0], GB)
+    assert abs(a[0] - (0.25 + 0.5) * GB) < 256 and abs(a[1] - 0.25 * GB) < 256
+    with pytest.raises(S.SwapNetError):
+        S.split_budget([0, GB], [1, 1], [1, 1], GB)
