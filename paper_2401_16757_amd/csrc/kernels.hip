@@ -945,16 +945,39 @@ hipError_t launch_maxpool(const void *x, void *y, int H, int W, int Cp, int Ho, 
 }
 
 // Mean over H*W per channel: one thread per channel, pixels summed in order.
+// Mean over H x W per channel.  A block is 16 groups of 8 channels (16-byte
+// loads; consecutive threads read consecutive chunks of one pixel) times 16
+// pixel lanes; lane l sums pixels l, l + 16, ... in order, then the 16 lane
+// sums are added in lane order.  Cp is a multiple of 8.
 __global__ void gavgpool_kernel(const _Float16 *x, _Float16 *y, int HW, int Cp) {
-    int c = blockIdx.x * blockDim.x + threadIdx.x;
-    if (c >= Cp) return;
-    float s = 0.0f;
-    for (int p = 0; p < HW; ++p) s += (float)x[(long)p * Cp + c];
-    y[c] = (_Float16)(s / (float)HW);
+    __shared__ float part[16][16][8];
+    const int g = threadIdx.x & 15, pl = threadIdx.x >> 4;
+    const int c8 = blockIdx.x * 16 + g;
+    const bool ok = c8 * 8 < Cp;
+    float acc[8] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
+    if (ok)
+        for (int p = pl; p < HW; p += 16) {
+            const h8 v = *(const h8 *)(x + (long)p * Cp + c8 * 8);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) acc[e] += (float)v[e];
+        }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) part[pl][g][e] = acc[e];
+    __syncthreads();
+    if (pl != 0 || !ok) return;
+    h8 o;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        float t = part[0][g][e];
+        for (int l = 1; l < 16; ++l) t += part[l][g][e];
+        o[e] = (_Float16)(t / (float)HW);
+    }
+    *(h8 *)(y + c8 * 8) = o;
 }
 
 hipError_t launch_gavgpool(const void *x, void *y, int HW, int Cp, hipStream_t s) {
-    hipLaunchKernelGGL(gavgpool_kernel, dim3((Cp + 63) / 64), dim3(64), 0, s, (const _Float16 *)x,
+    if (Cp % 8) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(gavgpool_kernel, dim3((Cp / 8 + 15) / 16), dim3(256), 0, s, (const _Float16 *)x,
                        (_Float16 *)y, HW, Cp);
     return hipGetLastError();
 }

@@ -96,6 +96,8 @@ CONV_SHAPES = [
     (64, 72, 9, 11, 3, 1, 2, 2), (32, 24, 13, 13, 3, 1, 4, 4), (256, 520, 7, 7, 1, 1, 0, 1),
     (24, 200, 15, 15, 1, 2, 0, 1), (512, 96, 7, 7, 3, 1, 1, 1), (64, 21, 40, 40, 1, 1, 0, 1),
     (128, 256, 56, 56, 1, 1, 0, 1), (64, 64, 56, 56, 3, 1, 1, 1),
+    # K-split with 16 tiles and a ragged last tile (partials added in-kernel)
+    (1024, 200, 14, 14, 3, 1, 1, 1),
 ]
 
 
