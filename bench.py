@@ -29,6 +29,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 MFMA_FP16_PEAK_TFLOPS = 2500.0     # MI355X dense fp16 MFMA
+PMC_INFERENCES = 5                 # resident inferences between the counter markers
 HBM_PEAK_GBS = 8000.0
 METRIC = "swapped/all-resident latency ratio at budget; H2D GB/s vs link peak; MFMA util"
 
@@ -67,7 +68,15 @@ def parse():
     ap.add_argument("--ablation", action="store_true",
                     help="also time the naive swapping modes (SN_OPT_NAIVE), untimed in `value`")
     ap.add_argument("--pmc-calibration", action="store_true",
-                    help="also run one 256 MiB device-to-device copy (counter calibration)")
+                    help="for counter runs: after the timed work, run a 256 MiB device-to-device "
+                         "copy (calibration and start marker), %d all-resident inferences and a "
+                         "64 MiB copy (end marker)" % PMC_INFERENCES)
+    ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="no GPU: summarise two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) of "
+                         "'bench.py --pmc-calibration' into profiles/<kernel>_<workload>_traffic.json")
+    ap.add_argument("--kernel", default=None,
+                    help="with --pmc-summary: the kernel (bench name); default: the roofline kernel "
+                         "of the workload's last bench line in FETCH_DIR/bench.json")
     return ap.parse_args()
 
 
@@ -194,19 +203,119 @@ def single_latency(torch, eng, xd, yd, n=10):
     return float(np.median(ts))
 
 
-def recorded_traffic(kernel):
-    """HBM bytes per dispatch of `kernel` from the committed counter summary
-    (profiles/*_traffic.json), or None when there is none or the kernel
-    source changed since the counters were taken."""
+def recorded_traffic(kernel, workload):
+    """HBM bytes per dispatch of `kernel` in `workload` from the committed
+    counter summary (profiles/*_traffic.json), or None when there is none or
+    the kernel source changed since the counters were taken."""
     import glob
     import hashlib
     src = os.path.join(ROOT, "paper_2401_16757_amd", "csrc", "kernels.hip")
     digest = hashlib.sha256(open(src, "rb").read()).hexdigest()
     for f in glob.glob(os.path.join(ROOT, "profiles", "*_traffic.json")):
         d = json.load(open(f))
-        if d.get("kernel") == kernel and d.get("kernels_hip_sha256") == digest:
+        if d.get("kernel") == kernel and d.get("workload") == workload and \
+                d.get("kernels_hip_sha256") == digest:
             return d["traffic_bytes_per_dispatch"]
     return None
+
+
+def pmc_window(torch, eng, xd, yd):
+    """Counter window: a 256 MiB device-to-device copy (its known bytes
+    calibrate the counters and mark the start), PMC_INFERENCES all-resident
+    inferences, then a 64 MiB copy (end marker).  The dispatches between the
+    markers are one known set of whole inferences."""
+    s = torch.cuda.current_stream()
+    src = torch.empty(256 << 20, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    src.fill_(3)
+    torch.cuda.synchronize()
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    for _ in range(PMC_INFERENCES):
+        eng.infer_dev(xd.data_ptr(), yd.data_ptr(), s.cuda_stream)
+    torch.cuda.synchronize()
+    dst[:64 << 20].copy_(src[:64 << 20])
+    torch.cuda.synchronize()
+    del src, dst
+
+
+def kernel_symbol(name):
+    """Demangled symbol of a conv kernel from its bench name."""
+    import re
+    m = re.match(r"conv3_mfma_(\d+)x(\d+)_s(\d+)_g(\d+)_(1x1|tap)$", name)
+    if m:
+        bm, bn, st, kg, kind = m.groups()
+        return "void sn::conv_mfma3_kernel<%s, %s, %s, %d, %s>(sn::ConvArgs)" % (
+            bm, bn, st, 0 if kind == "1x1" else 1, kg)
+    m = re.match(r"conv_mfma_(\d+)x(\d+)x(\d+)_w(\d)(\d)_gen$", name)
+    if m:
+        return "void sn::conv_mfma_kernel<%s, %s, %s, %s, %s, false>(sn::ConvArgs)" % m.groups()
+    raise ValueError("no symbol for kernel %r" % name)
+
+
+def read_counters(d, counter):
+    """Dispatches of a rocprofv3 --pmc CSV run: [(dispatch_id, kernel, value)]."""
+    import csv
+    import glob
+    files = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
+    if not files:
+        raise SystemExit("no *counter_collection.csv under %s" % d)
+    rows = {}
+    for f in files:
+        for r in csv.DictReader(open(f)):
+            if r["Counter_Name"] != counter:
+                continue
+            key = (f, int(r["Dispatch_Id"]))
+            k = rows.setdefault(key, [r["Kernel_Name"], 0.0])
+            k[1] += float(r["Counter_Value"])
+    return [(key[1], v[0], v[1]) for key, v in sorted(rows.items())]
+
+
+def window_average(rows, symbol, big_kib):
+    """Average counter value per dispatch of `symbol` between the two marker
+    copies, and the calibration copy's value (the first copy kernel whose
+    count reaches big_kib / 4, then the next one past 1/16 of it)."""
+    copies = [i for i, (_, k, v) in enumerate(rows) if "copyBuffer" in k and v >= big_kib / 4]
+    if not copies:
+        raise SystemExit("calibration copy not found")
+    i0 = copies[0]
+    cal = rows[i0][2]
+    ends = [i for i, (_, k, v) in enumerate(rows) if i > i0 and "copyBuffer" in k and v >= cal / 16]
+    if not ends:
+        raise SystemExit("end marker not found")
+    vals = [v for _, k, v in rows[i0 + 1:ends[0]] if k == symbol]
+    if not vals:
+        raise SystemExit("no dispatch of %s between the markers" % symbol)
+    return sum(vals) / len(vals), len(vals), cal
+
+
+def pmc_summary(a):
+    """Traffic of one kernel from two counter runs, scaled by the counters'
+    reading of the 256 MiB calibration copy (262144 KiB read and written)."""
+    import hashlib
+    fetch_dir, write_dir = a.pmc_summary
+    kernel = a.kernel
+    if kernel is None:
+        bj = json.load(open(os.path.join(fetch_dir, "bench.json")))
+        kernel = bj["roofline"]["kernel"]
+    sym = kernel_symbol(kernel)
+    ref_kib = 256 * 1024
+    f_avg, n, f_cal = window_average(read_counters(fetch_dir, "FETCH_SIZE"), sym, ref_kib)
+    w_avg, n2, w_cal = window_average(read_counters(write_dir, "WRITE_SIZE"), sym, ref_kib)
+    fs, ws = ref_kib / f_cal, ref_kib / w_cal
+    traffic = (f_avg * fs + w_avg * ws) * 1024
+    src = os.path.join(ROOT, "paper_2401_16757_amd", "csrc", "kernels.hip")
+    rec = {"kernel": kernel, "symbol": sym, "workload": a.workload,
+           "fetch_kib_per_dispatch_raw": round(f_avg, 1), "write_kib_per_dispatch_raw": round(w_avg, 1),
+           "dispatches": n, "inferences": PMC_INFERENCES,
+           "fetch_scale": round(fs, 4), "write_scale": round(ws, 4),
+           "traffic_bytes_per_dispatch": int(round(traffic)),
+           "kernels_hip_sha256": hashlib.sha256(open(src, "rb").read()).hexdigest()}
+    out = os.path.join(ROOT, "profiles", "%s_%s_traffic.json" % (kernel, a.workload))
+    with open(out, "w") as fh:
+        json.dump(rec, fh, indent=1)
+    print(json.dumps(rec))
+    print("wrote %s" % out, file=sys.stderr)
 
 
 def conv_flops(spec, c0, c1):
@@ -384,6 +493,8 @@ def bench_decoder(a, torch, S, W):
 
 def main():
     a = parse()
+    if a.pmc_summary:
+        return pmc_summary(a)
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if a.gpus != 1 or world != 1:
         print("bench.py: this engine runs on one GPU; --gpus %d is not supported "
@@ -440,14 +551,6 @@ def main():
 
     log("measuring pinned H2D peak")
     peak = measure_h2d_peak(torch)
-    if a.pmc_calibration:
-        src = torch.empty(256 << 20, dtype=torch.uint8, device="cuda")
-        dst = torch.empty_like(src)
-        src.fill_(3)
-        torch.cuda.synchronize()
-        dst.copy_(src)
-        torch.cuda.synchronize()
-        del src, dst
 
     log("timing %d swapped steps" % a.steps)
     sw_ms, sw_wall = timed_loop(torch, eng_sw, xd, yd, a.steps, a.warmup)
@@ -504,7 +607,7 @@ def main():
                     "frac": round(ach / peak_r, 5),
                     "flops_per_launch": round(fl / launches), "bytes_per_launch": round(by / launches),
                     "mfma_tflops": round(fl / (tms * 1e-3) / 1e12, 2),
-                    "traffic": recorded_traffic(name) if a.workload == "resnet50" else None}
+                    "traffic": recorded_traffic(name, a.workload)}
     mfma_util = (total_flops / (res_compute_ms * 1e-3) / 1e12) / MFMA_FP16_PEAK_TFLOPS \
         if res_compute_ms > 0 else None
 
@@ -569,6 +672,8 @@ def main():
     eng_sw.replan(budget)
     t2 = time.perf_counter()
     out["replan_ms"] = {"to_half_budget": round((t1 - t0) * 1e3, 2), "back": round((t2 - t1) * 1e3, 2)}
+    if a.pmc_calibration:
+        pmc_window(torch, eng_res, xd, yr)
     if not a.no_cpu_baseline:
         log("CPU oracle baseline (~%.0f s)" % a.cpu_seconds)
         out["cpu_baseline"] = cpu_baseline(net, wts, x, a.cpu_seconds)

@@ -237,6 +237,13 @@ enum sn_option {
                                    slab on the compute stream (no overlap, no
                                    graphs, no copy thread).  May be set after
                                    plan, between inferences                   */
+    SN_OPT_CONV_KERNEL = 11,    /* measurement only: 0 (default) chooses each
+                                   convolution's kernel from the layer shape;
+                                   k > 0 uses kernel variant k - 1
+                                   (sn_kernel_name) for every layer of that
+                                   variant's kind (1x1 / token GEMM, taps
+                                   with Cin_p % 64 == 0, or general).  Set
+                                   before sn_plan (or before sn_replan)       */
     SN_OPT_GRAPH = 4            /* 1 (default): the kernels of each slab of an
                                    image network are captured once per
                                    (input, output) buffer pair into one HIP

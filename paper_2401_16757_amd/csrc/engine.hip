@@ -98,6 +98,7 @@ struct sn_ctx {
     uint8_t *kv = nullptr;
     int partition = 0;                 // SN_OPT_PARTITION
     int naive = 0;                     // SN_OPT_NAIVE flags
+    int conv_force = 0;                // SN_OPT_CONV_KERNEL
     uint8_t *image_pageable = nullptr; // pageable copy of the image (SN_NAIVE_PAGEABLE)
     CostModel cost;                    // delay model (sn_set_cost_model / sn_calibrate)
     int64_t kv_bytes = 0;
@@ -293,6 +294,11 @@ extern "C" int sn_set_option(sn_ctx *c, int option, int64_t value) {
         if (value < 0 || value > 2) return fail(c, SN_E_INVALID, "partition must be 0, 1 or 2");
         c->partition = (int)value;
         return SN_OK;
+    case SN_OPT_CONV_KERNEL:
+        if (value < 0 || value > conv_kernel_count())
+            return fail(c, SN_E_INVALID, "conv kernel configuration out of range");
+        c->conv_force = (int)value;
+        return SN_OK;
     default:
         return fail(c, SN_E_INVALID, "unknown option");
     }
@@ -303,7 +309,7 @@ static void choose_layer_kernels(sn_ctx *c) {
         if (L.d.op != SN_OP_CONV2D) continue;
         const bool is1x1 = L.d.k == 1 && L.d.pad == 0;
         const int M = L.out_h * L.out_w;
-        ConvPlan p = conv_plan(M, L.d.c_out, L.K, L.cin_p, is1x1, true);
+        ConvPlan p = conv_plan(M, L.d.c_out, L.K, L.cin_p, is1x1, true, c->conv_force);
         L.kernel = p.kernel;
         L.ksplit = p.ksplit;
         L.kps = p.kps;
@@ -600,7 +606,7 @@ static int run_piece(sn_ctx *c, int pi, int n_tok, hipStream_t s) {
             a.relu = (d.flags & SN_FLAG_RELU) ? 1 : 0;
             a.swiglu = swiglu;
             // tile chosen from the whole layer, never from the piece
-            ConvPlan cp = conv_plan(M, (int)L.units * L.rows_per_unit, L.K, L.K, true, false);
+            ConvPlan cp = conv_plan(M, (int)L.units * L.rows_per_unit, L.K, L.K, true, false, c->conv_force);
             e = launch_conv(cp, a, s);
         }
         break;

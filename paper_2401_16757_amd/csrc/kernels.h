@@ -65,7 +65,9 @@ struct GemvArgs {
     int zero_end;       // if > n0 + units: zero outputs [n0 + units, zero_end)
 };
 
-ConvPlan conv_plan(int M, int N, int K, int cin_p, bool is1x1, bool allow_split);
+// force > 0 (measurement): use tile variant force - 1 wherever its kind
+// (general, 1x1 / token GEMM, taps with Cin_p % 64 == 0) is the layer's.
+ConvPlan conv_plan(int M, int N, int K, int cin_p, bool is1x1, bool allow_split, int force = 0);
 int64_t conv_workspace_bytes(const ConvPlan &p, int M, int N);
 int conv_kernel_count();
 const char *conv_kernel_name(int id);

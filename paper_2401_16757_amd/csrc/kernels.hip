@@ -421,12 +421,19 @@ __global__ __launch_bounds__(256 * KG) void conv_mfma3_kernel(ConvArgs a) {
     const int grp = KG > 1 ? wave >> 2 : 0;     // K group
     const int wm = (wave >> 1) & 1, wn = wave & 1;
 
-    // XCD-contiguous tile numbering
+    // XCD-contiguous tile numbering.  Tiles are numbered m-major (the tiles
+    // of one XCD share input rows) unless the weight rows outnumber the
+    // output pixels (late batch-1 layers): then n-major, so that each weight
+    // panel is fetched from HBM by one XCD rather than by every XCD that
+    // holds one of its output rows.
     const int nb = gridDim.x, bq = nb >> 3, br = nb & 7;
     const int xcd = blockIdx.x & 7;
     const int lb = xcd * bq + min(xcd, br) + (blockIdx.x >> 3);
     const int n_tiles = (a.n_cover + BN - 1) / BN;
-    const int m0 = (lb / n_tiles) * BM, nb0 = (lb % n_tiles) * BN;
+    const int m_tiles = (a.M + BM - 1) / BM;
+    const bool n_major = a.n_cover > a.M;
+    const int m0 = (n_major ? lb % m_tiles : lb / n_tiles) * BM;
+    const int nb0 = (n_major ? lb / m_tiles : lb % n_tiles) * BN;
 
     const i32x4 xr = make_srd(a.x, (long)a.H * a.W * a.Cin_p * 2);
     const i32x4 wr = make_srd(a.w, (long)a.N * a.K * 2);
@@ -726,11 +733,15 @@ static int find_variant(int bm, int bn, int kind) {
 // second pass over ksplit x M x N fp32 values).  1x1 convolutions, token
 // GEMMs and taps with Cin_p a multiple of 64 use the multi-stage kernel; the
 // rest (the first layer, Cin_p < 64) the single-buffered general one.
-ConvPlan conv_plan(int M, int N, int K, int cin_p, bool is1x1, bool allow_split) {
+ConvPlan conv_plan(int M, int N, int K, int cin_p, bool is1x1, bool allow_split, int force) {
     const int target = 256;
     const int kind = is1x1 ? 4 : (cin_p % 64 == 0 ? 5 : 0);
     ConvPlan p;
     p.kps = K;
+    if (force > 0 && force <= kNumConvVariants && kConvVariants[force - 1].kind == kind) {
+        p.kernel = force - 1;   // measurement: this variant wherever its kind applies
+        return p;
+    }
     if (kind == 0) {
         static const int tiles[][2] = {{128, 128}, {128, 64}, {64, 128}, {64, 64}};
         for (auto &t : tiles) {

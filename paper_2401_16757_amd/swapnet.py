@@ -31,6 +31,7 @@ OPT_COPY_STREAMS = 7
 OPT_PARTITION = 8
 OPT_SYNC = 9
 OPT_NAIVE = 10
+OPT_CONV_KERNEL = 11
 NAIVE_SEQUENTIAL, NAIVE_ALLOC, NAIVE_PAGEABLE, NAIVE_COPY_ASSEMBLY = 1, 2, 4, 8
 
 EXPORTS = ["sn_create", "sn_create_ex", "sn_add_block", "sn_plan", "sn_set_option", "sn_infer",
@@ -123,6 +124,15 @@ def load_library(path=LIB_PATH):
         f.argtypes = args
     _lib = lib
     return lib
+
+
+def conv_kernel_count():
+    """Number of convolution kernel variants (valid SN_OPT_CONV_KERNEL values
+    are 0 .. this count)."""
+    n = 0
+    while kernel_name(n) != "?":
+        n += 1
+    return n
 
 
 def kernel_name(kernel_id):
@@ -391,7 +401,7 @@ def output_shape(net):
 
 
 def build_engine(net, weights, budget=None, blocks=None, split_budget=None, host_only=False,
-                 timing=False, max_slab=0, partition=0, cost_model=None):
+                 timing=False, max_slab=0, partition=0, cost_model=None, conv_kernel=0):
     """Create, register and plan an engine for ``net``.  ``weights`` is a list
     of per-layer parameter dicts or a callable li -> dict.  ``cost_model``
     (a dict as returned by ``SwapNet.cost_model``) is set before planning;
@@ -405,6 +415,8 @@ def build_engine(net, weights, budget=None, blocks=None, split_budget=None, host
         eng.set_option(OPT_PARTITION, partition)
     if timing:
         eng.set_option(OPT_TIMING, int(timing))
+    if conv_kernel:
+        eng.set_option(OPT_CONV_KERNEL, conv_kernel)
     for a, b in (blocks or net.blocks):
         descs, blob = block_payload(net, weights, a, b)
         eng.add_block(descs, blob)

@@ -121,6 +121,45 @@ def test_conv_kernel_parity_and_slice_invariance(shape):
         assert np.array_equal(y.view(np.uint16), y2.view(np.uint16)), parts
 
 
+# every tile variant of the conv kernels, forced (SN_OPT_CONV_KERNEL) on the
+# shapes of its kind: strided and ragged 1x1, dilated and strided taps with
+# Cin_p a multiple of 64, K shorter than the stages in flight, output
+# channels not a multiple of the tile, weight rows outnumbering pixels
+FORCED_SHAPES = {
+    "1x1": [(64, 96, 9, 9, 1, 1, 0, 1), (40, 70, 11, 13, 1, 2, 0, 1), (512, 200, 7, 7, 1, 1, 0, 1),
+            (48, 40, 5, 3, 1, 1, 0, 1)],
+    "tap": [(64, 72, 11, 13, 3, 1, 2, 2), (128, 64, 7, 7, 3, 1, 1, 1), (64, 24, 6, 5, 3, 2, 1, 1),
+            (256, 300, 4, 4, 3, 1, 1, 1)],
+    "gen": [(3, 16, 13, 11, 3, 1, 1, 1), (16, 40, 9, 9, 3, 2, 1, 1), (8, 70, 12, 12, 7, 2, 3, 1)],
+}
+
+
+def _variant_kind(name):
+    return "1x1" if name.endswith("_1x1") else "tap" if name.endswith("_tap") else "gen"
+
+
+@pytest.mark.parametrize("variant", range(S.conv_kernel_count()))
+def test_forced_conv_variants(variant):
+    name = S.kernel_name(variant)
+    for shape in FORCED_SHAPES[_variant_kind(name)]:
+        ci, co, h, w, k, st, pad, dil = shape
+        print(f"[case] conv variant {name} shape {shape}", flush=True)
+        spec = W.LayerSpec(name="c", op="conv2d", src=0, dst=1, c_in=ci, c_out=co, h_in=h, w_in=w,
+                           k=k, stride=st, pad=pad, dilation=dil, relu=True, bn=True)
+        net = single_layer_net(spec)
+        wts = W.make_weights(net)
+        x = W.make_input(net)
+        ref = oracle.forward(net, wts, x)
+        y, _ = run(net, wts, x, budget=1 << 30, conv_kernel=variant + 1)
+        assert rel_err(y, ref) <= TOL, shape
+        wbytes = net.weight_bytes()
+        for parts in (2, 3):
+            y2, st2 = run(net, wts, x, budget=1 << 30, conv_kernel=variant + 1,
+                          split_budget=max(2 * wbytes // (parts + 1), 2048))
+            assert st2["n_slabs"] >= 2
+            assert np.array_equal(y.view(np.uint16), y2.view(np.uint16)), (shape, parts)
+
+
 LINEAR_SHAPES = [(256, 10, False), (2048, 1000, True), (25088, 4096, True), (4096, 37, False),
                  (520, 1003, True)]
 
