@@ -524,10 +524,13 @@ def main():
     if a.partition == 2:
         log("calibrating the delay model on the workload-block plan")
         with S.build_engine(net, wts, budget=budget) as cal:
+            cal.set_option(S.OPT_COPY_STREAMS, a.copy_streams)
             cal.calibrate(5)
             cm = cal.cost_model()
     log("planning swapped engine (budget %d B) and resident engine" % budget)
     eng_sw = S.build_engine(net, wts, budget=budget, partition=min(a.partition, 2), cost_model=cm)
+    # DMA queue use before the partition is chosen: it changes the per-DMA cost
+    eng_sw.set_option(S.OPT_COPY_STREAMS, a.copy_streams)
     tuned = None
     if a.partition == 3:
         log("choosing the partition by measurement (untimed)")

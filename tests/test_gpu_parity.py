@@ -246,14 +246,17 @@ def test_calibrated_searched_partition_matches_resident(name, kw, frac):
 
 
 @pytest.mark.parametrize("modes", [((2, 0),), ((2, 1),), ((1, 0),), ((0, 0),),
-                                   ((2, 1), (1, 0), (2, 0), (0, 0), (2, 1))])
+                                   ((2, 0, 2),), ((2, 1, 2),),
+                                   ((2, 1), (1, 0), (2, 0), (0, 0), (2, 1)),
+                                   ((2, 0, 2), (2, 1, 2), (2, 0, 1), (2, 0, 2), (1, 0, 2))])
 def test_back_to_back_inferences_with_cross_inference_prefetch(modes):
     # Several inferences queued without a host synchronisation: the next
     # inference's swap-ins of slabs that no earlier slab shares start while
     # the previous one still computes (waiting only for its `wrap` slabs).
     # Every output must equal a one-at-a-time inference of the same input,
     # bit for bit, in every swap-in mode (the copy thread with either kind of
-    # stream ordering, SN_OPT_SYNC 0 and 1) and when the modes alternate.
+    # stream ordering, SN_OPT_SYNC 0 and 1; one DMA queue or slabs alternating
+    # between two) and when the modes alternate.
     net, wts, x0, _ = net_case("resnet50", res=96)
     rng = np.random.default_rng(7)
     xs = [x0] + [rng.standard_normal(x0.shape).astype(np.float16) for _ in range(3)]
@@ -263,9 +266,10 @@ def test_back_to_back_inferences_with_cross_inference_prefetch(modes):
         want = [eng.infer(x) for x in xs]
         xd = [torch.from_numpy(x).cuda() for x in xs]
         s = torch.cuda.Stream()
-        for mode, sync in modes:
+        for mode, sync, *queues in modes:
             eng.set_option(S.OPT_SWAPIN, mode)
             eng.set_option(S.OPT_SYNC, sync)
+            eng.set_option(S.OPT_COPY_STREAMS, queues[0] if queues else 1)
             yd = [torch.empty(eng.out_shape, dtype=torch.float16, device="cuda") for _ in xs]
             with torch.cuda.stream(s):
                 for rep in range(2):
