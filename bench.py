@@ -67,6 +67,10 @@ def parse():
                     help="workgroups of the copy kernel (--swapin 0)")
     ap.add_argument("--ablation", action="store_true",
                     help="also time the naive swapping modes (SN_OPT_NAIVE), untimed in `value`")
+    ap.add_argument("--image-file", default=None, metavar="PATH",
+                    help="storage tier: write the swapped plan's image to PATH, swap in from it "
+                         "with direct I/O (sn_attach_image_file) and report the storage read "
+                         "rate against the file's raw O_DIRECT read rate")
     ap.add_argument("--pmc-calibration", action="store_true",
                     help="for counter runs: after the timed work, run a 256 MiB device-to-device "
                          "copy (calibration and start marker), %d all-resident inferences and a "
@@ -411,6 +415,94 @@ def cpu_baseline(net, wts, x, seconds):
 
 
 
+def direct_read_rate(path, reps=5):
+    """Median rate (GB/s) of reading the whole image file as the engine does:
+    one O_DIRECT read per slab (offsets and sizes from the file's header),
+    the page cache bypassed, no GPU work alongside."""
+    import mmap
+    import statistics
+    import struct
+    head = open(path, "rb").read(4096)
+    n = struct.unpack_from("<I", head, 12)[0]
+    hb = struct.unpack_from("<Q", head, 24)[0]
+    head = open(path, "rb").read(hb)
+    reqs = []
+    for i in range(n):
+        _, nbytes, off, _ = struct.unpack_from("<QQQQ", head, 32 + 32 * i)
+        reqs.append((off, (nbytes + 4095) // 4096 * 4096))
+    buf = mmap.mmap(-1, max(r[1] for r in reqs))
+    rates = []
+    for _ in range(reps):
+        try:
+            fd = os.open(path, os.O_RDONLY | os.O_DIRECT)
+        except OSError:
+            fd = os.open(path, os.O_RDONLY)
+        t0 = time.perf_counter()
+        total = 0
+        for off, ln in reqs:
+            total += os.preadv(fd, [memoryview(buf)[:ln]], off)
+        rates.append(total / (time.perf_counter() - t0) / 1e9)
+        os.close(fd)
+    buf.close()
+    return statistics.median(rates)
+
+
+def bench_storage(a, torch, S, net, wts, x, budget, frac_txt):
+    """Storage tier (direct block fetch): the swapped plan's image in a file,
+    every swap-in an O_DIRECT read into a pinned staging slot, then one DMA.
+    One step = one inference; the bound is the storage read rate."""
+    eng = S.build_engine(net, wts, budget=budget)
+    tuned = eng.tune(5) if a.partition == 3 else None
+    st = eng.stats()
+    eng_res = S.build_engine(net, wts, budget=st["image_bytes"] + 4096)
+    xd = torch.from_numpy(x).cuda()
+    yd = torch.empty(eng.out_shape, dtype=torch.float16, device="cuda")
+    yr = torch.empty(eng.out_shape, dtype=torch.float16, device="cuda")
+    log("host-memory swapped reference")
+    mem_ms, _ = timed_loop(torch, eng, xd, yd, a.steps, a.warmup)
+    y_mem = yd.clone()
+    log("writing the image file %s" % a.image_file)
+    eng.save_image(a.image_file)
+    raw = direct_read_rate(a.image_file)
+    eng.attach_image_file(a.image_file)
+    st2 = eng.stats()
+    log("timing %d swapped steps from the file" % a.steps)
+    r0 = st2["read_ms"]
+    sw_ms, sw_wall = timed_loop(torch, eng, xd, yd, a.steps, a.warmup)
+    read_ms = (eng.stats()["read_ms"] - r0) / (a.steps + a.warmup)
+    res_ms, _ = timed_loop(torch, eng_res, xd, yr, a.steps, a.warmup)
+    torch.cuda.synchronize()
+    bitwise = bool(torch.equal(yd.view(torch.int16), yr.view(torch.int16))) and \
+        bool(torch.equal(yd.view(torch.int16), y_mem.view(torch.int16)))
+    streamed = st["streamed_bytes"]
+    rate = streamed / (sw_ms * 1e-3) / 1e9
+    out = {
+        "metric": METRIC, "value": round(sw_ms / res_ms, 4), "unit": "x (swapped/resident latency)",
+        "n_gpus": 1, "steps": a.steps, "warmup": a.warmup, "ms_per_step": round(sw_ms, 4),
+        "higher_is_better": False, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f16 (fp32 accumulate)",
+        "data": "synthetic (seeded He-normal weights, folded BN, N(0,1) input)",
+        "config": {"workload": net.name, "batch": 1, "input": "x".join(map(str, net.input_shape)),
+                   "weight_bytes": net.weight_bytes(), "budget_bytes": budget,
+                   "budget_fraction": frac_txt, "slabs": st["n_slabs"],
+                   "partition": partition_name(a.partition if a.partition < 3 else 0, tuned),
+                   "weights": "image file, direct I/O" if st2["direct_io"] else "image file, buffered",
+                   "parallelism": "none (1 GPU)"},
+        "swapped_ms": round(sw_ms, 4), "resident_ms": round(res_ms, 4),
+        "swapped_from_host_memory_ms": round(mem_ms, 4), "swapped_wall_ms": round(sw_wall, 4),
+        "streamed_bytes_per_step": streamed,
+        "storage": {"bound": "storage_read", "achieved": round(rate, 3), "peak": round(raw, 3),
+                    "unit": "GB/s", "frac": round(rate / raw, 4) if raw > 0 else None,
+                    "read_ms_per_step": round(read_ms, 4)},
+        "host_weight_bytes": st2["host_weight_bytes"], "image_bytes": st["image_bytes"],
+        "direct_io": bool(st2["direct_io"]),
+        "swapped_equals_resident_bitwise": bitwise,
+    }
+    eng.close()
+    eng_res.close()
+    print(json.dumps(out), flush=True)
+
+
 def build_decoder(S, W, net, budget):
     """Register the decoder block by block, generating each block's weights
     just before it is added (the 13.5 GB of fp16 weights never coexist with
@@ -520,6 +612,8 @@ def main():
     frac_txt = {"resnet50": "1/2.32", "vgg16": "1/5.81", "fcn_resnet101": "1/3",
                 "tiny_cnn": "0.6"}[net.name] if a.budget_frac is None else "%.4f" % a.budget_frac
 
+    if a.image_file:
+        return bench_storage(a, torch, S, net, wts, x, budget, frac_txt)
     cm = None
     if a.partition == 2:
         log("calibrating the delay model on the workload-block plan")

@@ -388,6 +388,14 @@ typedef struct sn_stats {
                                    token networks)                             */
     int64_t output_bytes;       /* bytes sn_infer / sn_infer_tokens write to
                                    `output` / `logits`                         */
+    int64_t host_weight_bytes;  /* host memory holding weights: the pinned
+                                   image, or with an image file attached, the
+                                   two staging slots                           */
+    int32_t file_backed;        /* 1: swap-ins read the image file            */
+    int32_t direct_io;          /* 1: that file is read with O_DIRECT (no page
+                                   cache); 0: the file system refused it      */
+    double read_ms;             /* copy thread's time in file reads since the
+                                   file was attached (ms)                      */
 } sn_stats;
 int sn_get_stats(const sn_ctx *ctx, sn_stats *out);
 
@@ -428,8 +436,35 @@ int sn_get_piece(const sn_ctx *ctx, int j, sn_piece_info *out);
 /* Name of a kernel variant id (as reported in sn_piece_info.kernel), or "?". */
 const char *sn_kernel_name(int kernel);
 
-/* Pinned host image (after sn_plan): pointer and size, for inspection. */
+/* Pinned host image (after sn_plan): pointer and size, for inspection.
+ * SN_E_STATE once an image file is attached (the image is in the file). */
 int sn_get_image(const sn_ctx *ctx, const void **ptr, size_t *bytes);
+
+/* Storage tier: direct block fetch (Sec. 4.2.1).  The paper keeps the
+ * blocks in external storage and swaps a block in with direct I/O (no page
+ * cache, no second copy in memory).  sn_save_image writes the planned image
+ * (device layout, the slabs of this plan) to `path`: a header, then each
+ * slab at a 4 KiB-aligned offset, padded to 4 KiB, so that one O_DIRECT read
+ * fetches a slab.  Any context (host-only too) after sn_plan.  Errors:
+ * SN_E_STATE (not planned, or the image is already in a file),
+ * SN_E_INVALID (path NULL or not writable). */
+int sn_save_image(sn_ctx *ctx, const char *path);
+
+/* Swap in from the image file written by sn_save_image for this plan: the
+ * file is opened with O_DIRECT (buffered if the file system refuses it;
+ * sn_stats.direct_io), every slab is read back once and compared with the
+ * in-memory image, then the pinned image is released and host memory keeps
+ * two pinned staging slots of the largest slab (sn_stats.host_weight_bytes).
+ * Per inference the copy thread reads each slab into a free slot (the next
+ * slab is read while the current one is DMA'd and computed; after the last
+ * slab, the first slab of the next inference) and DMAs it into the arena.
+ * Results are bit-identical to the in-memory image.  Afterwards sn_replan,
+ * sn_tune, sn_calibrate, sn_get_image, SN_OPT_NAIVE and swap-in modes other
+ * than 2 return SN_E_STATE.  Errors: SN_E_STATE (not planned, resident
+ * plan, swap-in mode != 2 or naive flags set, already attached),
+ * SN_E_UNSUPPORTED (host-only context), SN_E_INVALID (path missing, not an
+ * image of this plan, content differs), SN_E_NOMEM, SN_E_HIP. */
+int sn_attach_image_file(sn_ctx *ctx, const char *path);
 
 const char *sn_last_error(const sn_ctx *ctx);
 

@@ -97,6 +97,21 @@ struct PlanTimes {
     double period = 0;    // per inference, back to back, steady state
 };
 
+// Storage tier (imagefile.cpp): the planned image in a file, each slab at a
+// kFileAlign-aligned offset, read back with direct I/O.
+constexpr int64_t kFileAlign = 4096;   // direct-I/O alignment of offsets, sizes, buffers
+int64_t image_file_slab_off(const PlanResult &plan, int i);
+int image_file_write(const std::string &path, const PlanResult &plan, const uint8_t *image,
+                     std::string &err);
+// Opens `path` (O_DIRECT when the file system allows it: `direct`), checks
+// its header against `plan` and returns the descriptor (-1 on error) and the
+// slabs' file offsets.
+int image_file_open(const std::string &path, const PlanResult &plan, std::vector<int64_t> &file_off,
+                    bool &direct, std::string &err);
+// Reads `bytes` rounded up to kFileAlign at `off` into `dst` (kFileAlign
+// aligned, room for the rounded size).
+int image_file_read(int fd, int64_t off, int64_t bytes, uint8_t *dst, std::string &err);
+
 // Host-only planning (no device calls).
 int validate_layers(std::vector<Layer> &layers, int from, std::vector<Slot> &slots,
                     std::string &err);

@@ -23,6 +23,8 @@
 #include <cstdio>
 #include <memory>
 #include <mutex>
+#include <sys/mman.h>
+#include <unistd.h>
 #include <thread>
 #include <cstdlib>
 #include <cstring>
@@ -112,6 +114,30 @@ struct sn_ctx {
     void *in_stage = nullptr, *out_stage = nullptr;
     float *ws = nullptr;               // split-K partial sums (outside the budget)
     int64_t ws_bytes = 0;
+
+    // storage tier (sn_attach_image_file): a reader thread reads the slabs
+    // of the image file in order, over and over, with direct I/O into two
+    // read slots (ordinary page-aligned memory: the runtime's pinned
+    // allocations cannot be the target of a direct read); the copy thread
+    // copies each into one of two pinned slots and DMAs it from there
+    int img_fd = -1;
+    bool img_direct = false;
+    std::vector<int64_t> file_off;     // per slab, in the file
+    std::vector<int> read_order;       // slabs with bytes, in order
+    uint8_t *rslot = nullptr;          // two read slots of slot_bytes (mmap)
+    uint8_t *staging = nullptr;        // two pinned slots of slot_bytes
+    int64_t slot_bytes = 0;
+    std::thread reader;
+    std::atomic<bool> reader_stop{false};
+    std::atomic<int64_t> reads_done{0};    // reads published (read k in slot k % 2)
+    std::atomic<int64_t> reads_taken{0};   // reads the copy thread is done with
+    std::atomic<int> read_error{0};
+    std::string read_err;
+    int64_t next_take = 0;             // copy thread: next read to consume
+    hipEvent_t slot_free[2] = {nullptr, nullptr};   // the DMA out of pinned slot
+    bool slot_busy[2] = {false, false};             // slot_free was recorded
+    int next_pin = 0;                  // copy thread: next pinned slot
+    std::atomic<int64_t> read_ns{0};   // reader: time in file reads
 
     int64_t in_bytes = 0, out_bytes = 0;
     std::vector<hipEvent_t> loaded, done;
@@ -257,6 +283,8 @@ extern "C" int sn_set_option(sn_ctx *c, int option, int64_t value) {
         return SN_OK;
     case SN_OPT_SWAPIN:
         if (value < 0 || value > 2) return fail(c, SN_E_INVALID, "swap-in mode must be 0, 1 or 2");
+        if (value != 2 && c->img_fd >= 0)
+            return fail(c, SN_E_STATE, "an image file is read by the copy thread (swap-in mode 2)");
         if (c->state == ST_PLANNED && c->have_prev) wait_copier_idle(c);
         if (c->swapin != (int)value) drop_graphs(c);
         c->swapin = (int)value;
@@ -287,6 +315,7 @@ extern "C" int sn_set_option(sn_ctx *c, int option, int64_t value) {
         return SN_OK;
     case SN_OPT_NAIVE:
         if (value < 0 || value > 15) return fail(c, SN_E_INVALID, "naive flags must be in [0, 15]");
+        if (value && c->img_fd >= 0) return fail(c, SN_E_STATE, "naive swapping reads the in-memory image");
         if (c->state == ST_PLANNED && c->have_prev) wait_copier_idle(c);
         c->naive = (int)value;
         return SN_OK;
@@ -666,6 +695,87 @@ static inline void spin_step(uint32_t &k) {
     else std::this_thread::yield();
 }
 
+// A wait step for a context that swaps in from an image file: every wait
+// there lasts about one file read (milliseconds), so after a short spin the
+// thread sleeps and leaves the cores to the I/O path.
+static inline void wait_step(const sn_ctx *c, uint32_t &k);
+
+static inline void wait_step(const sn_ctx *c, uint32_t &k) {
+    if (c->img_fd < 0) return spin_step(k);
+    if (++k < 256) cpu_relax();
+    else std::this_thread::sleep_for(std::chrono::microseconds(20));
+}
+
+// Storage tier.  Reader thread: read k (k = 0, 1, ...) fetches slab
+// read_order[k % n] into read slot k % 2 once read k - 2 has been taken.
+static void reader_main(sn_ctx *c) {
+    const int64_t n = (int64_t)c->read_order.size();
+    for (int64_t k = 0;; ++k) {
+        uint32_t w = 0;
+        while (c->reads_taken.load(std::memory_order_acquire) < k - 1) {
+            if (c->reader_stop.load()) return;
+            if (++w < 4096) __builtin_ia32_pause();
+            else std::this_thread::sleep_for(std::chrono::microseconds(20));
+        }
+        if (c->reader_stop.load()) return;
+        const int i = c->read_order[k % n];
+        std::string err;
+        const auto t0 = std::chrono::steady_clock::now();
+        const int rc = image_file_read(c->img_fd, c->file_off[i], c->plan.slabs[i].bytes,
+                                       c->rslot + (k & 1) * c->slot_bytes, err);
+        c->read_ns.fetch_add((int64_t)std::chrono::duration_cast<std::chrono::nanoseconds>(
+                                 std::chrono::steady_clock::now() - t0).count());
+        if (rc != SN_OK) {
+            c->read_err = err;
+            c->read_error.store(1, std::memory_order_release);
+            return;
+        }
+        c->reads_done.store(k + 1, std::memory_order_release);
+    }
+}
+
+// Copy thread: the bytes of slab i in a pinned slot (returned; -1 on error,
+// reported through copy_error).  Reads of other slabs (left by an aborted
+// inference) are skipped; the pinned slot is reused once its last DMA ended.
+static int take_slab(sn_ctx *c, int i) {
+    const int64_t n = (int64_t)c->read_order.size();
+    for (;;) {
+        const int64_t k = c->next_take;
+        uint32_t w = 0;
+        while (c->reads_done.load(std::memory_order_acquire) <= k) {
+            if (c->read_error.load(std::memory_order_acquire)) {
+                if (!c->copy_error.load()) {
+                    c->copy_err = c->read_err;
+                    c->copy_error.store(1);
+                }
+                return -1;
+            }
+            wait_step(c, w);
+        }
+        c->next_take = k + 1;
+        if (c->read_order[k % n] != i) {
+            c->reads_taken.store(k + 1, std::memory_order_release);
+            continue;
+        }
+        const int p = c->next_pin;
+        c->next_pin ^= 1;
+        hipError_t e = c->slot_busy[p] ? hipEventSynchronize(c->slot_free[p]) : hipSuccess;
+        c->slot_busy[p] = false;
+        if (e == hipSuccess)
+            memcpy(c->staging + p * c->slot_bytes, c->rslot + (k & 1) * c->slot_bytes,
+                   (size_t)c->plan.slabs[i].bytes);
+        c->reads_taken.store(k + 1, std::memory_order_release);
+        if (e != hipSuccess) {
+            if (!c->copy_error.load()) {
+                c->copy_err = std::string("staging slot: ") + hipGetErrorString(e);
+                c->copy_error.store(1);
+            }
+            return -1;
+        }
+        return p;
+    }
+}
+
 static void copier_main(sn_ctx *c) {
     const int ns = (int)c->plan.slabs.size();
     for (;;) {
@@ -710,14 +820,29 @@ static void copier_main(sn_ctx *c) {
                     aborted = true;
                     break;
                 }
-                spin_step(k);
+                wait_step(c, k);
             }
             if (aborted) break;
             hipError_t e = hipSuccess;
+            const uint8_t *src = c->image ? c->image + s.image_off : nullptr;
+            int slot = -1;
+            if (c->img_fd >= 0 && s.bytes) {
+                // storage tier: the slab was read (ahead, by the reader
+                // thread) from the file; copied into a pinned slot here
+                if ((slot = take_slab(c, i)) < 0) {
+                    aborted = true;
+                    break;
+                }
+                src = c->staging + slot * c->slot_bytes;
+            }
             if (e == hipSuccess && c->timing) e = hipEventRecord(c->t_in0[i], q);
             if (e == hipSuccess && s.bytes)
-                e = hipMemcpyAsync(c->arena + s.arena_off, c->image + s.image_off, (size_t)s.bytes,
-                                   hipMemcpyHostToDevice, q);
+                e = hipMemcpyAsync(c->arena + s.arena_off, src, (size_t)s.bytes, hipMemcpyHostToDevice, q);
+            if (e == hipSuccess && slot >= 0) {
+                // the pinned slot is free again once this DMA has read it
+                e = hipEventRecord(c->slot_free[slot], q);
+                c->slot_busy[slot] = e == hipSuccess;
+            }
             if (e == hipSuccess && c->timing) e = hipEventRecord(c->t_in1[i], q);
             if (e == hipSuccess)
                 e = c->sync == 1 ? hipStreamWriteValue64(q, c->lflag_dev + i, seq, 0)
@@ -934,7 +1059,7 @@ static int run_slabs(sn_ctx *c, int n_tok, hipStream_t cs, Pre pre, Post post, b
         // block that producer for good
         if (threaded) {
             uint32_t k = 0;
-            while (c->loaded_seq[i].load(std::memory_order_acquire) < seq) spin_step(k);
+            while (c->loaded_seq[i].load(std::memory_order_acquire) < seq) wait_step(c, k);
             if (c->copy_error.load()) return abort_copies(fail(c, SN_E_HIP, c->copy_err));
         }
         hipError_t e = hipSuccess;
@@ -1177,6 +1302,8 @@ extern "C" int sn_reset(sn_ctx *c) {
 extern "C" int sn_replan(sn_ctx *c, size_t budget_bytes) {
     if (!c) return SN_E_INVALID;
     if (c->state != ST_PLANNED) return fail(c, SN_E_STATE, "sn_replan before sn_plan");
+    if (c->img_fd >= 0) return fail(c, SN_E_STATE, "the image is in a file (sn_attach_image_file)");
+
     const int64_t B = budget_bytes ? (int64_t)budget_bytes : c->budget;
     if (B < kAlign) return fail(c, SN_E_INVALID, "budget must be at least 256 bytes");
     const int64_t split = c->split_explicit ? c->split_budget : B;
@@ -1596,6 +1723,8 @@ static int time_back_to_back(sn_ctx *c, double &t) {
 extern "C" int sn_tune(sn_ctx *c, int reps, double *times_s) {
     int rc = check_ready(c, c ? c->token : false);
     if (rc) return rc;
+    if (c->img_fd >= 0) return fail(c, SN_E_STATE, "the image is in a file (sn_attach_image_file)");
+
     if (reps < 1 || reps > 64) return fail(c, SN_E_INVALID, "reps must be in [1, 64]");
     if (c->token && c->pos >= c->max_seq) return fail(c, SN_E_INVALID, "KV cache full (max_seq reached)");
     if (times_s)
@@ -1634,6 +1763,8 @@ extern "C" int sn_tune(sn_ctx *c, int reps, double *times_s) {
 extern "C" int sn_calibrate(sn_ctx *c, int reps) {
     int rc = check_ready(c, c ? c->token : false);
     if (rc) return rc;
+    if (c->img_fd >= 0) return fail(c, SN_E_STATE, "the image is in a file (sn_attach_image_file)");
+
     if (reps < 1 || reps > 64) return fail(c, SN_E_INVALID, "reps must be in [1, 64]");
     if (c->token && c->pos >= c->max_seq) return fail(c, SN_E_INVALID, "KV cache full (max_seq reached)");
     CostModel m = c->cost;
@@ -1665,6 +1796,10 @@ extern "C" int sn_get_stats(const sn_ctx *c, sn_stats *o) {
     o->resident = c->plan.resident ? 1 : 0;
     o->n_infers = c->n_infers;
     o->last_ms = c->last_ms;
+    o->host_weight_bytes = c->img_fd >= 0 ? 4 * c->slot_bytes : c->plan.image_bytes;
+    o->file_backed = c->img_fd >= 0 ? 1 : 0;
+    o->direct_io = c->img_fd >= 0 && c->img_direct ? 1 : 0;
+    o->read_ms = c->read_ns.load() * 1e-6;
     return SN_OK;
 }
 
@@ -1711,7 +1846,7 @@ extern "C" int sn_get_piece(const sn_ctx *c, int j, sn_piece_info *o) {
 
 extern "C" int sn_get_image(const sn_ctx *c, const void **ptr, size_t *bytes) {
     if (!c || !ptr || !bytes) return SN_E_INVALID;
-    if (c->state != ST_PLANNED) return SN_E_STATE;
+    if (c->state != ST_PLANNED || !c->image) return SN_E_STATE;
     *ptr = c->image;
     *bytes = (size_t)c->plan.image_bytes;
     return SN_OK;
@@ -1727,6 +1862,10 @@ extern "C" const char *sn_last_error(const sn_ctx *c) {
 extern "C" void sn_destroy(sn_ctx *c) {
     if (!c) return;
     stop_copier(c);
+    if (c->reader.joinable()) {
+        c->reader_stop.store(true);
+        c->reader.join();
+    }
     if (!c->host_only) {
         if (c->comp_s) hipStreamSynchronize(c->comp_s);
         if (c->copy_s) hipStreamSynchronize(c->copy_s);
@@ -1738,8 +1877,11 @@ extern "C" void sn_destroy(sn_ctx *c) {
         if (c->t_start) hipEventDestroy(c->t_start);
         if (c->fork) hipEventDestroy(c->fork);
         if (c->ev_end) hipEventDestroy(c->ev_end);
+        for (hipEvent_t e : c->slot_free)
+            if (e) hipEventDestroy(e);
         drop_graphs(c);
         if (c->image) hipHostFree(c->image);
+        if (c->staging) hipHostFree(c->staging);
         if (c->table_host) hipHostFree(c->table_host);
         if (c->sig_host) hipHostFree(c->sig_host);
         if (c->lflag_host) hipHostFree(c->lflag_host);
@@ -1753,6 +1895,95 @@ extern "C" void sn_destroy(sn_ctx *c) {
     } else {
         free(c->image);
     }
+    if (c->img_fd >= 0) close(c->img_fd);
+    if (c->rslot) munmap(c->rslot, (size_t)(2 * c->slot_bytes));
     free(c->image_pageable);
     delete c;
+}
+
+// ---------------------------------------------------------------------------
+// Storage tier (Sec. 4.2.1, direct block fetch): the planned image in a file,
+// read back slab by slab with direct I/O into a two-slot pinned staging ring
+// by the copy thread, each slab then DMA'd into the arena as before.
+// ---------------------------------------------------------------------------
+extern "C" int sn_save_image(sn_ctx *c, const char *path) {
+    if (!c || !path || !*path) return SN_E_INVALID;
+    if (c->state != ST_PLANNED) return fail(c, SN_E_STATE, "sn_save_image before sn_plan");
+    if (!c->image) return fail(c, SN_E_STATE, "the image is in a file already");
+    std::string err;
+    int rc = image_file_write(path, c->plan, c->image, err);
+    return rc ? fail(c, rc, err) : SN_OK;
+}
+
+extern "C" int sn_attach_image_file(sn_ctx *c, const char *path) {
+    if (!c || !path || !*path) return SN_E_INVALID;
+    if (c->state != ST_PLANNED) return fail(c, SN_E_STATE, "sn_attach_image_file before sn_plan");
+    if (c->host_only) return fail(c, SN_E_UNSUPPORTED, "host-only context");
+    if (c->img_fd >= 0) return fail(c, SN_E_STATE, "an image file is attached already");
+    if (c->plan.resident) return fail(c, SN_E_STATE, "resident plan: nothing is swapped in");
+    if (c->swapin != 2 || c->naive)
+        return fail(c, SN_E_STATE, "an image file is read by the copy thread (swap-in mode 2, no naive flags)");
+    // no inference in flight
+    wait_copier_idle(c);
+    if (c->have_prev) HIP_TRY(c, hipEventSynchronize(c->ev_end));
+    if (c->copy_s) HIP_TRY(c, hipStreamSynchronize(c->copy_s));
+    if (c->copy_s2) HIP_TRY(c, hipStreamSynchronize(c->copy_s2));
+    std::string err;
+    bool direct = false;
+    std::vector<int64_t> off;
+    const int fd = image_file_open(path, c->plan, off, direct, err);
+    if (fd < 0) return fail(c, SN_E_INVALID, err);
+    int64_t slot = kFileAlign;
+    for (const Slab &s : c->plan.slabs) slot = std::max(slot, align_up(s.bytes, kFileAlign));
+    uint8_t *staging = nullptr;
+    void *rs = mmap(nullptr, (size_t)(2 * slot), PROT_READ | PROT_WRITE, MAP_PRIVATE | MAP_ANONYMOUS, -1, 0);
+    uint8_t *rslot = rs == MAP_FAILED ? nullptr : (uint8_t *)rs;
+    hipError_t e = hipHostMalloc((void **)&staging, (size_t)(2 * slot), 0);
+    int rc = SN_OK;
+    if (e != hipSuccess || !rslot) {
+        rc = fail(c, SN_E_NOMEM, std::string("staging allocation: ") +
+                                     (rslot ? hipGetErrorString(e) : strerror(errno)));
+    } else {
+        // the file must hold exactly the in-memory image: read every slab back
+        for (size_t i = 0; i < c->plan.slabs.size() && !rc; ++i) {
+            const Slab &s = c->plan.slabs[i];
+            if ((rc = image_file_read(fd, off[i], s.bytes, rslot, err))) {
+                rc = fail(c, rc, err);
+            } else if (memcmp(rslot, c->image + s.image_off, (size_t)s.bytes) != 0) {
+                rc = fail(c, SN_E_INVALID, "image file " + std::string(path) + ": slab " +
+                                               std::to_string(i) + " differs from the plan's image");
+            }
+        }
+    }
+    for (int k = 0; k < 2 && !rc; ++k)
+        if (!c->slot_free[k] && (e = hipEventCreateWithFlags(&c->slot_free[k], hipEventDisableTiming)) != hipSuccess)
+            rc = fail(c, SN_E_HIP, hipGetErrorString(e));
+    if (rc) {
+        if (staging) hipHostFree(staging);
+        if (rslot) munmap(rslot, (size_t)(2 * slot));
+        close(fd);
+        return rc;
+    }
+    // host memory now holds the read and pinned slots instead of the image
+    hipHostFree(c->image);
+    c->image = c->image_dev = nullptr;
+    free(c->image_pageable);
+    c->image_pageable = nullptr;
+    c->img_fd = fd;
+    c->img_direct = direct;
+    c->file_off = off;
+    c->read_order.clear();
+    for (int i = 0; i < (int)c->plan.slabs.size(); ++i)
+        if (c->plan.slabs[i].bytes) c->read_order.push_back(i);
+    c->rslot = rslot;
+    c->staging = staging;
+    c->slot_bytes = slot;
+    c->slot_busy[0] = c->slot_busy[1] = false;
+    c->next_pin = 0;
+    c->next_take = 0;
+    c->reads_done.store(0);
+    c->reads_taken.store(0);
+    c->read_ns.store(0);
+    if (!c->read_order.empty()) c->reader = std::thread(reader_main, c);
+    return SN_OK;
 }

@@ -331,9 +331,28 @@ __device__ __forceinline__ void dma16_to_lds(i32x4 srd, unsigned lds_base, unsig
         : "memory");
 }
 
+// Bias and residual of eight consecutive output channels n .. n+7 of output
+// pixel m, loaded ahead of the epilogue (`ok`: the 16-byte path of finish8
+// applies, and the values are in `b` / `r`).
+struct Pre8 {
+    h8 b, r;
+    bool ok;
+};
+
+__device__ __forceinline__ void prefetch8(const ConvArgs &a, int m, int n, Pre8 &p) {
+    p.ok = a.ksplit == 1 && !a.swiglu && m < a.M && (a.n0 % 8) == 0 && n + 8 <= a.N;
+    p.b = zero_h8();
+    p.r = zero_h8();
+    if (!p.ok) return;
+    if (a.bias) p.b = *(const h8 *)((const _Float16 *)a.bias + n);
+    if (a.res) p.r = *(const h8 *)((const _Float16 *)a.res + (long)m * a.ldy + a.n0 + n);
+}
+
 // Bias, residual, ReLU or SwiGLU and the fp16 rounding of eight consecutive
-// weight rows n .. n+7 of output pixel m (or their fp32 K-split partials).
-__device__ __forceinline__ void finish8(const ConvArgs &a, int m, int n, float (&v)[8]) {
+// weight rows n .. n+7 of output pixel m (or their fp32 K-split partials);
+// `pre` (optional) holds bias and residual already loaded by prefetch8.
+__device__ __forceinline__ void finish8(const ConvArgs &a, int m, int n, float (&v)[8],
+                                        const Pre8 *pre = nullptr) {
     if (a.ksplit > 1) {
         float *ws = a.ws + ((long)blockIdx.y * a.M + m) * a.N;
         if (n + 8 <= a.N && (a.N % 4) == 0) {
@@ -360,6 +379,19 @@ __device__ __forceinline__ void finish8(const ConvArgs &a, int m, int n, float (
         return;
     }
     const long idx = (long)m * a.ldy + a.n0 + n;
+    if (pre && pre->ok) {
+        h8 o;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            // the same additions, in the same order, as the paths below
+            float x = v[e];
+            if (a.bias) x += (float)pre->b[e];
+            if (a.res) x += (float)pre->r[e];
+            o[e] = (_Float16)(a.relu ? fmaxf(x, 0.0f) : x);
+        }
+        *(h8 *)(yg + idx) = o;
+        return;
+    }
     if ((a.n0 % 8) == 0 && n + 8 <= a.N) {
         if (bg) {
             h8 b = *(const h8 *)(bg + n);
@@ -597,13 +629,32 @@ __global__ __launch_bounds__(256 * KG) void conv_mfma3_kernel(ConvArgs a) {
         if (rem > decltype(J)::value) step(t + decltype(J)::value, J);
     });
 
+    // epilogue: 32 rows of the tile at a time through LDS (TM x 2 rounds,
+    // at most one group of eight channels per thread and round); the bias
+    // and residual of every round are loaded first, so their memory latency
+    // overlaps the last K tiles instead of being paid once per round
+    constexpr int ITEMS = 32 * BN / 8;
+    constexpr int IPT = (ITEMS + NT - 1) / NT;   // items per thread and round
+    Pre8 pre[TM][2][IPT];
+#pragma unroll
+    for (int u = 0; u < IPT; ++u) {
+        const int q = tid + u * NT;
+        const int r = q / (BN / 8), n = nb0 + (q % (BN / 8)) * 8;
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int wmm = 0; wmm < 2; ++wmm) {
+                pre[i][wmm][u].ok = false;
+                if (q < ITEMS) prefetch8(a, m0 + wmm * WTM + i * 32 + r, n, pre[i][wmm][u]);
+            }
+    }
+
     // the loads issued past the end of the K range (zeros) have landed and
     // every wave is done with the operand stages before the epilogue reuses
     // them
     wait_vmcnt<0>();
 
-    // epilogue: 32 rows of the tile at a time through LDS; the K groups'
-    // partial sums are added in group order
+    // the K groups' partial sums are added in group order
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
 #pragma unroll
@@ -620,18 +671,21 @@ __global__ __launch_bounds__(256 * KG) void conv_mfma3_kernel(ConvArgs a) {
             }
             __syncthreads();
             const int mb = m0 + wmm * WTM + i * 32;
-            for (int q = tid; q < 32 * BN / 8; q += NT) {
+#pragma unroll
+            for (int u = 0; u < IPT; ++u) {
+                const int q = tid + u * NT;
                 const int r = q / (BN / 8), nl = (q % (BN / 8)) * 8;
                 const int m = mb + r, n = nb0 + nl;
-                if (m >= a.M || n >= a.n_cover) continue;
-                float v[8];
+                if (q < ITEMS && m < a.M && n < a.n_cover) {
+                    float v[8];
 #pragma unroll
-                for (int e = 0; e < 8; ++e) v[e] = stc[r * LDC + nl + e];
+                    for (int e = 0; e < 8; ++e) v[e] = stc[r * LDC + nl + e];
 #pragma unroll
-                for (int g = 1; g < KG; ++g)
+                    for (int g = 1; g < KG; ++g)
 #pragma unroll
-                    for (int e = 0; e < 8; ++e) v[e] += stc[(g * 32 + r) * LDC + nl + e];
-                finish8(a, m, n, v);
+                        for (int e = 0; e < 8; ++e) v[e] += stc[(g * 32 + r) * LDC + nl + e];
+                    finish8(a, m, n, v, &pre[i][wmm][u]);
+                }
             }
         }
     }

@@ -38,7 +38,7 @@ EXPORTS = ["sn_create", "sn_create_ex", "sn_add_block", "sn_plan", "sn_set_optio
            "sn_infer_dev", "sn_infer_tokens", "sn_reset", "sn_get_stats", "sn_get_slab",
            "sn_get_piece", "sn_get_image", "sn_kernel_name", "sn_last_error", "sn_destroy",
            "sn_set_cost_model", "sn_get_cost_model", "sn_calibrate", "sn_predict", "sn_replan",
-           "sn_tune", "sn_split_budget"]
+           "sn_tune", "sn_split_budget", "sn_save_image", "sn_attach_image_file"]
 COST_KEYS = ("alpha", "beta", "gamma", "kappa", "gate", "wake", "slab_ex")
 
 
@@ -60,7 +60,9 @@ class SnStats(C.Structure):
                 ("activation_bytes", C.c_int64), ("kv_bytes", C.c_int64),
                 ("table_bytes", C.c_int64), ("n_slabs", C.c_int32), ("n_pieces", C.c_int32),
                 ("n_layers", C.c_int32), ("resident", C.c_int32), ("n_infers", C.c_int64),
-                ("last_ms", C.c_double), ("input_bytes", C.c_int64), ("output_bytes", C.c_int64)]
+                ("last_ms", C.c_double), ("input_bytes", C.c_int64), ("output_bytes", C.c_int64),
+                ("host_weight_bytes", C.c_int64), ("file_backed", C.c_int32),
+                ("direct_io", C.c_int32), ("read_ms", C.c_double)]
 
 
 class SnSlabInfo(C.Structure):
@@ -116,6 +118,7 @@ def load_library(path=LIB_PATH):
         "sn_split_budget": (I, [I, C.POINTER(C.c_int64), C.POINTER(C.c_double),
                                 C.POINTER(C.c_double), C.c_int64, C.POINTER(C.c_int64)]),
         "sn_predict": (I, [P, C.POINTER(C.c_double), C.POINTER(C.c_double)]),
+        "sn_save_image": (I, [P, C.c_char_p]), "sn_attach_image_file": (I, [P, C.c_char_p]),
         "sn_last_error": (C.c_char_p, [P]), "sn_destroy": (None, [P]),
     }
     for name, (res, args) in sig.items():
@@ -310,6 +313,14 @@ class SwapNet:
         lat, per = C.c_double(), C.c_double()
         self._check(self.lib.sn_predict(self.ctx, C.byref(lat), C.byref(per)))
         return lat.value, per.value
+
+    def save_image(self, path):
+        """Write the planned image to ``path`` (sn_save_image)."""
+        return self._check(self.lib.sn_save_image(self.ctx, os.fsencode(path)))
+
+    def attach_image_file(self, path):
+        """Swap in from the image file at ``path`` (sn_attach_image_file)."""
+        return self._check(self.lib.sn_attach_image_file(self.ctx, os.fsencode(path)))
 
     def image(self):
         ptr, n = C.c_void_p(), C.c_size_t()

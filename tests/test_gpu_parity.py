@@ -280,6 +280,73 @@ def test_back_to_back_inferences_with_cross_inference_prefetch(modes):
                 assert np.array_equal(yd[i].cpu().numpy().view(np.uint16), want[i].view(np.uint16)), (mode, i)
 
 
+@pytest.mark.parametrize("name,kw", [("tiny_cnn", {}), ("resnet50", {"res": 96})])
+def test_image_file_swapin_matches_memory(tmp_path, name, kw):
+    # Storage tier (direct block fetch): after sn_attach_image_file every
+    # swap-in reads its slab from the file into a staging slot, then DMAs it.
+    # Outputs must equal the in-memory image's bit for bit: host path, device
+    # path, several inferences queued back to back.
+    net, wts, x0, ref = net_case(name, **kw)
+    rng = np.random.default_rng(11)
+    xs = [x0] + [rng.standard_normal(x0.shape).astype(np.float16) for _ in range(2)]
+    path = str(tmp_path / "image.bin")
+    with S.build_engine(net, wts) as eng:
+        st0 = eng.stats()
+        assert not st0["resident"] and st0["n_slabs"] >= 2
+        want = [eng.infer(x) for x in xs]
+        eng.save_image(path)
+        eng.attach_image_file(path)
+        st = eng.stats()
+        print(f"[case] {name}: {st['n_slabs']} slabs, direct_io={st['direct_io']}, "
+              f"host weight bytes {st['host_weight_bytes']} of {st['image_bytes']}", flush=True)
+        assert st["file_backed"] == 1
+        # two read slots and two pinned slots of the largest slab (4 KiB pages)
+        slot = -(-max(s["bytes"] for s in eng.slabs()) // 4096) * 4096
+        assert st["host_weight_bytes"] == 4 * slot
+        for rep in range(2):
+            for x, w in zip(xs, want):
+                assert np.array_equal(eng.infer(x).view(np.uint16), w.view(np.uint16)), rep
+        xd = [torch.from_numpy(x).cuda() for x in xs]
+        yd = [torch.empty(eng.out_shape, dtype=torch.float16, device="cuda") for _ in xs]
+        s = torch.cuda.Stream()
+        with torch.cuda.stream(s):
+            for rep in range(2):
+                for i in range(len(xs)):
+                    eng.infer_dev(xd[i].data_ptr(), yd[i].data_ptr(), s.cuda_stream)
+        s.synchronize()
+        for i in range(len(xs)):
+            assert np.array_equal(yd[i].cpu().numpy().view(np.uint16), want[i].view(np.uint16)), i
+        assert eng.stats()["read_ms"] > 0
+        # calls that need the in-memory image are refused
+        for call in (lambda: eng.replan(), lambda: eng.tune(1), lambda: eng.calibrate(1),
+                     lambda: eng.image(), lambda: eng.set_option(S.OPT_SWAPIN, 1),
+                     lambda: eng.set_option(S.OPT_NAIVE, 1), lambda: eng.attach_image_file(path)):
+            with pytest.raises(S.SwapNetError) as e:
+                call()
+            assert e.value.code == S.SN_E_STATE
+        # still running from the file afterwards
+        assert np.array_equal(eng.infer(x0).view(np.uint16), want[0].view(np.uint16))
+    assert rel_err(want[0], ref) <= TOL
+    # a file of another plan, and a file whose slab bytes differ, are refused;
+    # the engine keeps swapping from memory
+    with S.build_engine(net, wts, budget=int(st0["image_bytes"] * 0.3)) as other:
+        assert other.stats()["n_slabs"] != st0["n_slabs"]
+        with pytest.raises(S.SwapNetError) as e:
+            other.attach_image_file(path)
+        assert e.value.code == S.SN_E_INVALID
+    raw = bytearray(open(path, "rb").read())
+    raw[-5000] ^= 0x5A if len(raw) > 5000 else 0
+    raw[4096 + 17] ^= 0x01
+    bad = str(tmp_path / "bad.bin")
+    open(bad, "wb").write(bytes(raw))
+    with S.build_engine(net, wts) as eng:
+        with pytest.raises(S.SwapNetError) as e:
+            eng.attach_image_file(bad)
+        assert e.value.code == S.SN_E_INVALID
+        assert eng.stats()["file_backed"] == 0
+        assert np.array_equal(eng.infer(x0).view(np.uint16), want[0].view(np.uint16))
+
+
 def small_decoder(**kw):
     a = dict(n_layers=2, d=128, heads=4, ffn=160, vocab=300, max_seq=48, prompt=24, gen=8)
     a.update(kw)

@@ -35,7 +35,7 @@ def test_library_exports_every_declared_symbol():
 def test_struct_sizes_match_header_layout():
     # sn_layer: 19 int32 + 2 float + 4 int64 = 76 + 8 + 32 -> 120 with alignment
     assert C.sizeof(S.SnLayer) == 120
-    assert C.sizeof(S.SnStats) == 7 * 8 + 4 * 4 + 8 + 8 + 2 * 8
+    assert C.sizeof(S.SnStats) == 7 * 8 + 4 * 4 + 8 + 8 + 2 * 8 + 8 + 2 * 4 + 8
 
 
 def plan_of(name, budget=None, **kw):
