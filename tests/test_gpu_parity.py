@@ -493,6 +493,29 @@ def test_decoder_replan_mid_generation():
     assert np.array_equal(runs[0].view(np.uint32), runs[1].view(np.uint32))
 
 
+def test_decoder_generation_from_image_file(tmp_path):
+    # the storage tier under a token network: prefill and decode steps with
+    # every layer block read from the image file give the same logits bits
+    net = small_decoder()
+    wts = W.make_weights(net)
+    prompt = W.make_input(net)
+    lb = sum(l.weight_bytes() for l in net.layers[1:8])
+    path = str(tmp_path / "decoder.img")
+    runs = []
+    for from_file in (False, True):
+        with S.build_engine(net, wts, budget=2 * lb) as eng:
+            assert not eng.stats()["resident"]
+            if from_file:
+                eng.save_image(path)
+                eng.attach_image_file(path)
+                assert eng.stats()["file_backed"] == 1
+            rows = [eng.infer_tokens(prompt)]
+            for _ in range(5):
+                rows.append(eng.infer_tokens(np.array([int(np.argmax(rows[-1]))], np.int32)))
+            runs.append(np.stack(rows))
+    assert np.array_equal(runs[0].view(np.uint32), runs[1].view(np.uint32))
+
+
 def test_decoder_long_context_split_attention():
     # 200-token prompt: single-token steps attend over 200+ cached positions,
     # which the attention kernel splits over several blocks (per-chunk
