@@ -24,6 +24,14 @@ Operator definitions (standard; the paper uses stock framework operators):
   rmsnorm  : v / sqrt(mean(v^2) + eps) * gain
   attention: RoPE (rotate-half, theta), causal softmax(q k^T / sqrt(hd)) v
   gateup   : silu(W1 x) * (W3 x)
+
+Pins (the tests of the oracle, independent of this code): brute-force loops
+on tiny shapes, torch float64 operators, closed forms (identity / one-hot
+kernels, tap counts, constants and ramps, RoPE as a complex rotation, unit
+RMS), BN folding against explicit batch norm, independent torch builds of
+every network, and partition invariance.  Whole-network output values
+against the paper: parity unpinned (the paper prints no forward-pass
+values, weights or inputs).
 """
 from __future__ import annotations
 
@@ -192,7 +200,9 @@ def forward(net, weights, x):
 
 def forward_blocks(net, weights, x, blocks):
     """Run the network block by block, in order; each block's layers read
-    their inputs from the activations left by the previous blocks."""
+    their inputs from the activations left by the previous blocks (Sec. 3,
+    "Basic Idea": the blocks execute one by one; Sec. 6, partition of
+    blocks: the output of one block feeds the next)."""
     assert net.kind == "cnn"
     assert blocks[0][0] == 0 and blocks[-1][1] == len(net.layers)
     assert all(blocks[i][1] == blocks[i + 1][0] for i in range(len(blocks) - 1))
