@@ -463,7 +463,7 @@ def bench_storage(a, torch, S, net, wts, x, budget, frac_txt):
     y_mem = yd.clone()
     log("writing the image file %s" % a.image_file)
     eng.save_image(a.image_file)
-    raw = direct_read_rate(a.image_file)
+    raw_before = direct_read_rate(a.image_file)
     eng.attach_image_file(a.image_file)
     st2 = eng.stats()
     log("timing %d swapped steps from the file" % a.steps)
@@ -472,6 +472,9 @@ def bench_storage(a, torch, S, net, wts, x, budget, frac_txt):
     read_ms = (eng.stats()["read_ms"] - r0) / (a.steps + a.warmup)
     res_ms, _ = timed_loop(torch, eng_res, xd, yr, a.steps, a.warmup)
     torch.cuda.synchronize()
+    # the disk's sustained rate: a read burst right after the file was
+    # written runs faster than the same reads a few seconds later
+    raw = direct_read_rate(a.image_file)
     bitwise = bool(torch.equal(yd.view(torch.int16), yr.view(torch.int16))) and \
         bool(torch.equal(yd.view(torch.int16), y_mem.view(torch.int16)))
     streamed = st["streamed_bytes"]
@@ -493,6 +496,7 @@ def bench_storage(a, torch, S, net, wts, x, budget, frac_txt):
         "streamed_bytes_per_step": streamed,
         "storage": {"bound": "storage_read", "achieved": round(rate, 3), "peak": round(raw, 3),
                     "unit": "GB/s", "frac": round(rate / raw, 4) if raw > 0 else None,
+                    "peak_right_after_write": round(raw_before, 3),
                     "read_ms_per_step": round(read_ms, 4)},
         "host_weight_bytes": st2["host_weight_bytes"], "image_bytes": st["image_bytes"],
         "direct_io": bool(st2["direct_io"]),
