@@ -160,6 +160,44 @@ def test_forced_conv_variants(variant):
             assert np.array_equal(y.view(np.uint16), y2.view(np.uint16)), (shape, parts)
 
 
+def _random_conv_shapes(n, seed):
+    rng = np.random.default_rng(seed)
+    out = []
+    for _ in range(n):
+        k = int(rng.choice([1, 3, 3, 5, 7]))
+        ci = int(rng.choice([3, 8, 13, 32, 64, 72, 128, 200, 256]))
+        co = int(rng.choice([5, 16, 33, 64, 100, 128, 257]))
+        h, w = int(rng.integers(3, 30)), int(rng.integers(3, 30))
+        st = int(rng.choice([1, 1, 2]))
+        dil = int(rng.choice([1, 1, 2])) if k > 1 else 1
+        pad = int(rng.integers(0, dil * (k // 2) + 1))
+        if (h + 2 * pad - dil * (k - 1) - 1) < 0 or (w + 2 * pad - dil * (k - 1) - 1) < 0:
+            pad = dil * (k // 2)
+        out.append((ci, co, h, w, k, st, pad, dil))
+    return out
+
+
+@pytest.mark.parametrize("shape", _random_conv_shapes(16, 2024))
+def test_random_conv_shapes(shape):
+    # seeded random convolutions (ragged channels and sizes, any padding,
+    # strides, dilations): parity with the oracle and bit-identity of the
+    # layer cut into two and three channel slices
+    ci, co, h, w, k, st, pad, dil = shape
+    print(f"[case] random conv {shape}", flush=True)
+    spec = W.LayerSpec(name="c", op="conv2d", src=0, dst=1, c_in=ci, c_out=co, h_in=h, w_in=w,
+                       k=k, stride=st, pad=pad, dilation=dil, relu=bool(co % 2), bn=True)
+    net = single_layer_net(spec)
+    wts = W.make_weights(net)
+    x = W.make_input(net)
+    ref = oracle.forward(net, wts, x)
+    y, _ = run(net, wts, x, budget=1 << 30)
+    assert rel_err(y, ref) <= TOL
+    wbytes = net.weight_bytes()
+    for parts in (2, 3):
+        y2, st2 = run(net, wts, x, budget=1 << 30, split_budget=max(2 * wbytes // (parts + 1), 2048))
+        assert np.array_equal(y.view(np.uint16), y2.view(np.uint16)), parts
+
+
 LINEAR_SHAPES = [(256, 10, False), (2048, 1000, True), (25088, 4096, True), (4096, 37, False),
                  (520, 1003, True)]
 
