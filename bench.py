@@ -71,6 +71,9 @@ def parse():
                     help="storage tier: write the swapped plan's image to PATH, swap in from it "
                          "with direct I/O (sn_attach_image_file) and report the storage read "
                          "rate against the file's raw O_DIRECT read rate")
+    ap.add_argument("--link-sweep", action="store_true",
+                    help="only measure the pinned host -> device copy rate for sizes 4 KiB .. "
+                         "1 GiB (median of 20 each; one JSON line per size)")
     ap.add_argument("--pmc-calibration", action="store_true",
                     help="for counter runs: after the timed work, run a 256 MiB device-to-device "
                          "copy (calibration and start marker), %d all-resident inferences and a "
@@ -112,6 +115,34 @@ def measure_h2d_peak(torch, sizes=(64 << 20, 256 << 20), reps=8):
         best = max(best, float(np.median(rates)))
     del h, d
     return best
+
+
+def link_sweep(torch, reps=20):
+    """Pinned host -> device copy rate by size, 4 KiB .. 1 GiB: median of
+    `reps` timed copies (hipMemcpyAsync via torch, HIP events)."""
+    n_max = 1 << 30
+    h = torch.empty(n_max, dtype=torch.uint8, pin_memory=True)
+    h.fill_(1)
+    d = torch.empty(n_max, dtype=torch.uint8, device="cuda")
+    s = torch.cuda.current_stream()
+    n = 4 << 10
+    while n <= n_max:
+        for _ in range(2):
+            d[:n].copy_(h[:n], non_blocking=True)
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(s)
+            d[:n].copy_(h[:n], non_blocking=True)
+            e1.record(s)
+            e1.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        ms = float(np.median(ts))
+        print(json.dumps({"bytes": n, "median_ms": round(ms, 5), "gbps": round(n / (ms * 1e-3) / 1e9, 2),
+                          "sdma": os.environ.get("HSA_ENABLE_SDMA", "default")}), flush=True)
+        n *= 4
+    del h, d
 
 
 def measure_copy_chain(torch, sizes, reps=5):
@@ -606,6 +637,8 @@ def main():
     # (recorded on the current stream) bracket it
     stream = torch.cuda.Stream()
     torch.cuda.set_stream(stream)
+    if a.link_sweep:
+        return link_sweep(torch)
     if a.workload == "decoder7b":
         return bench_decoder(a, torch, S, W)
     net = W.get_network(a.workload)
