@@ -372,9 +372,16 @@ static int setup_plan_resources(sn_ctx *c) {
     const int ns = (int)c->plan.slabs.size();
     c->loaded.assign(ns, nullptr);
     c->done.assign(ns, nullptr);
+    // loaded[i] (DMA -> kernels) and done[i] (kernels -> next DMA into the
+    // region) only order work on this device: the DMA writes HBM directly and
+    // the kernels that read it are dispatched with their own acquire, so
+    // these markers skip the system-scope cache writeback / invalidate
+    // (≈ 2.3 µs per DMA on the copy queue).  ev_end and the pinned-slot
+    // events, which the host waits on, keep it.
+    const unsigned dev_only = hipEventDisableTiming | hipEventDisableSystemFence;
     for (int i = 0; i < ns; ++i) {
-        HIP_TRY(c, hipEventCreateWithFlags(&c->loaded[i], hipEventDisableTiming));
-        HIP_TRY(c, hipEventCreateWithFlags(&c->done[i], hipEventDisableTiming));
+        HIP_TRY(c, hipEventCreateWithFlags(&c->loaded[i], dev_only));
+        HIP_TRY(c, hipEventCreateWithFlags(&c->done[i], dev_only));
     }
     c->t_in0.assign(ns, nullptr);
     c->t_in1.assign(ns, nullptr);
