@@ -437,11 +437,16 @@ __global__ __launch_bounds__(256 * KG) void conv_mfma3_kernel(ConvArgs a) {
     constexpr int KPG = 4 / KG;                 // 16-wide K steps per group per K tile
     constexpr int STAGE = (BM + BN) * 64;       // halves per stage
     constexpr int LDC = BN + 4;                 // fp32 staging row
+    // epilogue rows staged per round: the whole tile when the K groups'
+    // fp32 partials of all BM rows fit in the operand stages, else 64 or 32
+    constexpr int RR = KG * BM * LDC * 4 <= S * STAGE * 2 ? BM : KG * 64 * LDC * 4 <= S * STAGE * 2 ? 64 : 32;
+    constexpr int ROUNDS = BM / RR;
     static_assert(KG == 1 || KG == 2 || KG == 4, "1, 2 or 4 K groups");
     static_assert(kSplit || QA + QB == NW, "load groups per wave");
     static_assert(S >= 3 && S <= 8, "3 to 8 stages");
     static_assert((S - 1) * NI < 64, "vmcnt range");
-    static_assert(KG * 32 * LDC * 4 <= S * STAGE * 2, "staging tile exceeds LDS");
+    static_assert(KG * RR * LDC * 4 <= S * STAGE * 2 && BM % RR == 0 && RR % 32 == 0,
+                  "staging tile exceeds LDS");
     // S operand stages; the epilogue reuses the space for the fp32 partials
     __shared__ __attribute__((aligned(16))) _Float16 smem[S * STAGE];
     auto buf = [&](auto J) -> _Float16 * { return smem + (decltype(J)::value % S) * STAGE; };
@@ -629,25 +634,22 @@ __global__ __launch_bounds__(256 * KG) void conv_mfma3_kernel(ConvArgs a) {
         if (rem > decltype(J)::value) step(t + decltype(J)::value, J);
     });
 
-    // epilogue: 32 rows of the tile at a time through LDS (TM x 2 rounds,
-    // at most one group of eight channels per thread and round); the bias
-    // and residual of every round are loaded first, so their memory latency
-    // overlaps the last K tiles instead of being paid once per round
-    constexpr int ITEMS = 32 * BN / 8;
+    // epilogue: RR rows of the tile per round through LDS (one round where
+    // the tile fits: two barriers, one item of eight channels per thread);
+    // the bias and residual of every round are loaded first, so their memory
+    // latency overlaps the last K tiles instead of being paid once per round
+    constexpr int ITEMS = RR * BN / 8;
     constexpr int IPT = (ITEMS + NT - 1) / NT;   // items per thread and round
-    Pre8 pre[TM][2][IPT];
+    Pre8 pre[ROUNDS][IPT];
 #pragma unroll
-    for (int u = 0; u < IPT; ++u) {
-        const int q = tid + u * NT;
-        const int r = q / (BN / 8), n = nb0 + (q % (BN / 8)) * 8;
+    for (int rd = 0; rd < ROUNDS; ++rd)
 #pragma unroll
-        for (int i = 0; i < TM; ++i)
-#pragma unroll
-            for (int wmm = 0; wmm < 2; ++wmm) {
-                pre[i][wmm][u].ok = false;
-                if (q < ITEMS) prefetch8(a, m0 + wmm * WTM + i * 32 + r, n, pre[i][wmm][u]);
-            }
-    }
+        for (int u = 0; u < IPT; ++u) {
+            const int q = tid + u * NT;
+            const int r = q / (BN / 8), n = nb0 + (q % (BN / 8)) * 8;
+            pre[rd][u].ok = false;
+            if (q < ITEMS) prefetch8(a, m0 + rd * RR + r, n, pre[rd][u]);
+        }
 
     // the loads issued past the end of the K range (zeros) have landed and
     // every wave is done with the operand stages before the epilogue reuses
@@ -656,12 +658,13 @@ __global__ __launch_bounds__(256 * KG) void conv_mfma3_kernel(ConvArgs a) {
 
     // the K groups' partial sums are added in group order
 #pragma unroll
-    for (int i = 0; i < TM; ++i) {
+    for (int rd = 0; rd < ROUNDS; ++rd) {
+        __syncthreads();
 #pragma unroll
-        for (int wmm = 0; wmm < 2; ++wmm) {
-            __syncthreads();
-            if (wm == wmm) {
-                float *dst = stc + grp * 32 * LDC;
+        for (int i = 0; i < TM; ++i) {
+            const int rb = wm * WTM + i * 32;   // first tile row of this 32-row block
+            if (rb / RR == rd) {
+                float *dst = stc + (grp * RR + rb % RR) * LDC;
 #pragma unroll
                 for (int j = 0; j < TN; ++j)
 #pragma unroll
@@ -669,23 +672,23 @@ __global__ __launch_bounds__(256 * KG) void conv_mfma3_kernel(ConvArgs a) {
                         dst[((v >> 2) * 8 + (lane >> 5) * 4 + (v & 3)) * LDC + wn * WTN + j * 32 + lrow] =
                             acc[i][j][v];
             }
-            __syncthreads();
-            const int mb = m0 + wmm * WTM + i * 32;
+        }
+        __syncthreads();
+        const int mb = m0 + rd * RR;
 #pragma unroll
-            for (int u = 0; u < IPT; ++u) {
-                const int q = tid + u * NT;
-                const int r = q / (BN / 8), nl = (q % (BN / 8)) * 8;
-                const int m = mb + r, n = nb0 + nl;
-                if (q < ITEMS && m < a.M && n < a.n_cover) {
-                    float v[8];
+        for (int u = 0; u < IPT; ++u) {
+            const int q = tid + u * NT;
+            const int r = q / (BN / 8), nl = (q % (BN / 8)) * 8;
+            const int m = mb + r, n = nb0 + nl;
+            if (q < ITEMS && m < a.M && n < a.n_cover) {
+                float v[8];
 #pragma unroll
-                    for (int e = 0; e < 8; ++e) v[e] = stc[r * LDC + nl + e];
+                for (int e = 0; e < 8; ++e) v[e] = stc[r * LDC + nl + e];
 #pragma unroll
-                    for (int g = 1; g < KG; ++g)
+                for (int g = 1; g < KG; ++g)
 #pragma unroll
-                        for (int e = 0; e < 8; ++e) v[e] += stc[(g * 32 + r) * LDC + nl + e];
-                    finish8(a, m, n, v, &pre[i][wmm][u]);
-                }
+                    for (int e = 0; e < 8; ++e) v[e] += stc[(g * RR + r) * LDC + nl + e];
+                finish8(a, m, n, v, &pre[rd][u]);
             }
         }
     }
