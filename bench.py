@@ -58,9 +58,10 @@ def parse():
                          "calibrated on this GPU (on the workload-block plan, untimed); "
                          "3 (default): the fastest of 0, 1, 2 measured on this GPU "
                          "(sn_tune, untimed)")
-    ap.add_argument("--sync", type=int, default=0, choices=[0, 1],
+    ap.add_argument("--sync", type=int, default=2, choices=[0, 1, 2],
                     help="copy thread ordering: 0 events + signal kernels, "
-                         "1 stream write/wait of values in mapped memory")
+                         "1 stream write/wait of values in mapped memory, "
+                         "2 ROCr SDMA copies with a gate kernel polling each slab's completion signal")
     ap.add_argument("--copy-streams", type=int, default=1, choices=[1, 2],
                     help="DMA queues used by the copy thread (consecutive slabs alternate)")
     ap.add_argument("--swapin-blocks", type=int, default=None,
@@ -761,7 +762,7 @@ def main():
                    "budget_fraction": frac_txt, "user_blocks": len(net.blocks),
                    "slabs": st["n_slabs"],
                    "partition": partition_name(a.partition, tuned),
-                   "sync": ["events", "stream values"][a.sync],
+                   "sync": ["events", "stream values", "rocr copies + gate kernels"][a.sync],
                    "parallelism": "none (1 GPU)"},
         "swapped_ms": round(sw_ms, 4), "resident_ms": round(res_ms, 4),
         "swapped_latency_ms": round(sw_lat, 4), "resident_latency_ms": round(res_lat, 4),

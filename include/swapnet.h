@@ -224,8 +224,18 @@ enum sn_option {
                                    partitions 0 and 1 as candidates too      */
     SN_OPT_SYNC = 9,            /* copy-thread mode (SN_OPT_SWAPIN 2): how
                                    the copy and compute streams order each
-                                   other.  0: hipEvents for "slab loaded" and
-                                   a one-thread kernel that bumps a mapped
+                                   other.  2 (default): each swap-in is a
+                                   ROCr SDMA copy (hsa_amd_memory_async_copy)
+                                   with a completion signal per slab, and a
+                                   one-wave gate kernel ahead of the slab's
+                                   kernels polls that signal (bounded wait:
+                                   after 2 s it flags an error that the next
+                                   call reports as SN_E_HIP); "slab
+                                   computed" as in 0.  Runs with per-slab
+                                   timing (SN_OPT_TIMING) and contexts with
+                                   an image file use mode 0's ordering.
+                                   0: hipEvents for "slab loaded" and a
+                                   one-thread kernel that bumps a mapped
                                    counter for "slab computed"; 1: stream
                                    writes / waits of 64-bit values in mapped
                                    memory (hipStreamWriteValue64 /

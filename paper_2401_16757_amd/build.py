@@ -56,7 +56,7 @@ def build(verbose=False):
             continue
         objs.append(obj)
     tmp = LIB + ".tmp"
-    _run([hipcc, "-shared", "-fPIC", "--offload-arch=" + ARCH, "-o", tmp] + objs, verbose)
+    _run([hipcc, "-shared", "-fPIC", "--offload-arch=" + ARCH, "-o", tmp] + objs + ["-lhsa-runtime64"], verbose)
     os.replace(tmp, LIB)
     return LIB
 

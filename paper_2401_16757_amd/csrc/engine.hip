@@ -14,6 +14,8 @@
 //             back, the range is simply reused.
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
+#include <hsa/hsa.h>
+#include <hsa/hsa_ext_amd.h>
 
 #include <algorithm>
 #include <atomic>
@@ -92,7 +94,19 @@ struct sn_ctx {
     unsigned long long *sig_host = nullptr, *sig_dev = nullptr;
     // per-slab "swap-in done" values written by the copy stream (SN_OPT_SYNC 1)
     unsigned long long *lflag_host = nullptr, *lflag_dev = nullptr;
-    int sync = 0;                      // SN_OPT_SYNC
+    int sync = 2;                      // SN_OPT_SYNC
+    // SN_OPT_SYNC 2: swap-ins through ROCr (hsa_amd_memory_async_copy on the
+    // SDMA engine), one completion signal per slab, polled on the device by a
+    // gate kernel ahead of the slab's kernels.  `rocr_run`: the inference in
+    // flight uses that path (set by the calling thread before the copy thread
+    // is released, read by both for that inference).
+    bool hsa_up = false;
+    hsa_agent_t hsa_gpu{0}, hsa_cpu{0};
+    std::vector<hsa_signal_t> dsig;
+    std::vector<const int64_t *> dsig_val;
+    int *gate_err_host = nullptr, *gate_err_dev = nullptr;
+    std::atomic<bool> rocr_run{false};
+    unsigned long long gate_limit = 200000000ull;   // 2 s of the 100 MHz counter
     std::atomic<int> copy_error{0};
     std::string copy_err;
     uint8_t *act = nullptr;
@@ -199,6 +213,90 @@ static hipError_t ensure_own_queue_stream(hipStream_t *s, int device) {
         if (e_ != hipSuccess)                                                                    \
             return fail(ctx, SN_E_HIP, std::string(#call) + ": " + hipGetErrorString(e_));        \
     } while (0)
+
+// SN_OPT_SYNC 2.  ROCr agents of this context's GPU (matched to the HIP
+// device by PCI domain, bus and device) and of the host.
+struct AgentSearch {
+    uint32_t domain, bdf;
+    int gpus;
+    hsa_agent_t gpu, any_gpu, cpu;
+};
+
+static hsa_status_t agent_cb(hsa_agent_t a, void *d) {
+    AgentSearch *q = (AgentSearch *)d;
+    hsa_device_type_t t;
+    if (hsa_agent_get_info(a, HSA_AGENT_INFO_DEVICE, &t) != HSA_STATUS_SUCCESS) return HSA_STATUS_SUCCESS;
+    if (t == HSA_DEVICE_TYPE_CPU && !q->cpu.handle) q->cpu = a;
+    if (t != HSA_DEVICE_TYPE_GPU) return HSA_STATUS_SUCCESS;
+    ++q->gpus;
+    if (!q->any_gpu.handle) q->any_gpu = a;
+    uint32_t bdf = 0, dom = 0;
+    if (hsa_agent_get_info(a, (hsa_agent_info_t)HSA_AMD_AGENT_INFO_BDFID, &bdf) == HSA_STATUS_SUCCESS &&
+        hsa_agent_get_info(a, (hsa_agent_info_t)HSA_AMD_AGENT_INFO_DOMAIN, &dom) == HSA_STATUS_SUCCESS &&
+        (bdf & ~7u) == q->bdf && dom == q->domain && !q->gpu.handle)
+        q->gpu = a;
+    return HSA_STATUS_SUCCESS;
+}
+
+static int ensure_hsa(sn_ctx *c) {
+    if (c->hsa_up) return SN_OK;
+    if (hsa_init() != HSA_STATUS_SUCCESS) return fail(c, SN_E_HIP, "ROCr: hsa_init failed");
+    c->hsa_up = true;   // balanced by hsa_shut_down when the context is destroyed
+    int bus = 0, dev = 0, dom = 0;
+    HIP_TRY(c, hipDeviceGetAttribute(&bus, hipDeviceAttributePciBusId, c->device));
+    HIP_TRY(c, hipDeviceGetAttribute(&dev, hipDeviceAttributePciDeviceId, c->device));
+    HIP_TRY(c, hipDeviceGetAttribute(&dom, hipDeviceAttributePciDomainID, c->device));
+    AgentSearch q{(uint32_t)dom, ((uint32_t)bus << 8) | ((uint32_t)dev << 3), 0, {0}, {0}, {0}};
+    if (hsa_iterate_agents(agent_cb, &q) != HSA_STATUS_SUCCESS) return fail(c, SN_E_HIP, "ROCr: agent query failed");
+    c->hsa_gpu = q.gpu.handle ? q.gpu : (q.gpus == 1 ? q.any_gpu : hsa_agent_t{0});
+    c->hsa_cpu = q.cpu;
+    if (!c->hsa_gpu.handle || !c->hsa_cpu.handle)
+        return fail(c, SN_E_UNSUPPORTED, "ROCr: this GPU's or the host's agent not found");
+    return SN_OK;
+}
+
+// One completion signal per slab (value 0 = the slab's last copy landed),
+// created GPU-only so that its value can be read by the gate kernel; and the
+// gates' time-out flag in mapped host memory.
+static int setup_rocr_signals(sn_ctx *c) {
+    if (!c->dsig.empty() || c->plan.resident || c->host_only) return SN_OK;
+    int rc = ensure_hsa(c);
+    if (rc) return rc;
+    if (!c->gate_err_host) {
+        HIP_TRY(c, hipHostMalloc((void **)&c->gate_err_host, sizeof(int), hipHostMallocMapped));
+        *(volatile int *)c->gate_err_host = 0;
+        HIP_TRY(c, hipHostGetDevicePointer((void **)&c->gate_err_dev, c->gate_err_host, 0));
+    }
+    const int ns = (int)c->plan.slabs.size();
+    c->dsig.assign(ns, hsa_signal_t{0});
+    c->dsig_val.assign(ns, nullptr);
+    for (int i = 0; i < ns; ++i) {
+        if (hsa_amd_signal_create(0, 0, nullptr, HSA_AMD_SIGNAL_AMD_GPU_ONLY, &c->dsig[i]) != HSA_STATUS_SUCCESS)
+            return fail(c, SN_E_HIP, "ROCr: signal creation failed");
+        volatile hsa_signal_value_t *vp = nullptr;
+        if (hsa_amd_signal_value_pointer(c->dsig[i], &vp) != HSA_STATUS_SUCCESS || !vp)
+            return fail(c, SN_E_HIP, "ROCr: signal value not addressable");
+        c->dsig_val[i] = (const int64_t *)vp;
+    }
+    return SN_OK;
+}
+
+static void release_rocr_signals(sn_ctx *c) {
+    // gate kernels read these signals: the last inference's end follows them
+    if (!c->dsig.empty() && c->have_prev && c->ev_end) hipEventSynchronize(c->ev_end);
+    for (hsa_signal_t x : c->dsig)
+        if (x.handle) hsa_signal_destroy(x);
+    c->dsig.clear();
+    c->dsig_val.clear();
+}
+
+// A gate that ran out of time leaves its flag set: reported (and cleared)
+// by the next call that checks the copy thread.
+static bool take_gate_error(sn_ctx *c) {
+    if (!c->gate_err_host || !*(volatile int *)c->gate_err_host) return false;
+    *(volatile int *)c->gate_err_host = 0;
+    return true;
+}
 
 // ---------------------------------------------------------------------------
 // Create / add / plan
@@ -308,10 +406,11 @@ extern "C" int sn_set_option(sn_ctx *c, int option, int64_t value) {
         c->max_slab = value;
         return SN_OK;
     case SN_OPT_SYNC:
-        if (value != 0 && value != 1) return fail(c, SN_E_INVALID, "sync must be 0 or 1");
+        if (value < 0 || value > 2) return fail(c, SN_E_INVALID, "sync must be 0, 1 or 2");
         if (c->state == ST_PLANNED && c->have_prev) wait_copier_idle(c);
         if ((int)value != c->sync) drop_graphs(c);   // the graphs hold the signal kernels
         c->sync = (int)value;
+        if (value == 2 && c->state == ST_PLANNED) return setup_rocr_signals(c);
         return SN_OK;
     case SN_OPT_NAIVE:
         if (value < 0 || value > 15) return fail(c, SN_E_INVALID, "naive flags must be in [0, 15]");
@@ -421,6 +520,10 @@ static int setup_plan_resources(sn_ctx *c) {
                                  hipHostMallocMapped));
         memset(c->lflag_host, 0, ns * sizeof(unsigned long long));
         HIP_TRY(c, hipHostGetDevicePointer((void **)&c->lflag_dev, c->lflag_host, 0));
+        if (c->sync == 2) {
+            int rc = setup_rocr_signals(c);
+            if (rc) return rc;
+        }
         start_copier(c);
     }
     if (c->plan.resident) {
@@ -450,6 +553,7 @@ static void release_plan_resources(sn_ctx *c) {
     if (c->sig_host) hipHostFree(c->sig_host);
     if (c->lflag_host) hipHostFree(c->lflag_host);
     c->sig_host = c->sig_dev = c->lflag_host = c->lflag_dev = nullptr;
+    release_rocr_signals(c);
     c->stop = false;
     c->requested = 0;
     c->seq = c->tseq = 0;
@@ -804,6 +908,8 @@ static void copier_main(sn_ctx *c) {
             if (c->stop) return;
             seq = c->handled.load() + 1;
         }
+        // set before this inference was released to this thread
+        const bool rocr = c->rocr_run.load(std::memory_order_relaxed);
         bool aborted = false;
         for (int i = 0; i < ns && !aborted; ++i) {
             const Slab &s = c->plan.slabs[i];
@@ -842,6 +948,21 @@ static void copier_main(sn_ctx *c) {
                 }
                 src = c->staging + slot * c->slot_bytes;
             }
+            if (rocr) {
+                // the slab's signal drops from 1 to 0 when the SDMA engine has
+                // written the last byte; the gate kernel waits for that
+                hsa_signal_store_relaxed(c->dsig[i], s.bytes ? 1 : 0);
+                if (s.bytes && hsa_amd_memory_async_copy(c->arena + s.arena_off, c->hsa_gpu, src, c->hsa_cpu,
+                                                         (size_t)s.bytes, 0, nullptr, c->dsig[i]) != HSA_STATUS_SUCCESS) {
+                    hsa_signal_store_relaxed(c->dsig[i], 0);   // nothing left to wait for
+                    if (!c->copy_error.load()) {
+                        c->copy_err = "swap-in DMA: hsa_amd_memory_async_copy failed";
+                        c->copy_error.store(1);
+                    }
+                }
+                c->loaded_seq[i].store(seq, std::memory_order_release);
+                continue;
+            }
             if (e == hipSuccess && c->timing) e = hipEventRecord(c->t_in0[i], q);
             if (e == hipSuccess && s.bytes)
                 e = hipMemcpyAsync(c->arena + s.arena_off, src, (size_t)s.bytes, hipMemcpyHostToDevice, q);
@@ -877,6 +998,8 @@ static int check_copier(sn_ctx *c) {
     if (!c->copier.joinable()) return SN_OK;
     wait_copier_idle(c);
     if (c->copy_error.exchange(0)) return fail(c, SN_E_HIP, c->copy_err);
+    if (take_gate_error(c))
+        return fail(c, SN_E_HIP, "swap-in gate: a DMA did not land within the gate's time limit");
     return SN_OK;
 }
 
@@ -1020,11 +1143,19 @@ static int run_slabs(sn_ctx *c, int n_tok, hipStream_t cs, Pre pre, Post post, b
     const bool prev_complete = c->complete_seq.load() == c->seq;
     c->wrap_ok_nt = prev_complete;
     const uint64_t run = ++c->seq;
+    // ROCr swap-ins and device-side gates (SN_OPT_SYNC 2); per-slab timing
+    // and an image file keep the event path (timing brackets the copies with
+    // events, and a pinned staging slot is reused once its copy's event fired)
+    const bool rocr = threaded && c->sync == 2 && !c->timing && c->img_fd < 0;
+    if (rocr && c->dsig.size() != (size_t)ns) return fail(c, SN_E_STATE, "ROCr swap-in signals not set up");
     if (threaded) {
         // the copy thread must be done with the previous inference's events
         // before they are recorded again
         wait_copier_idle(c);
         if (c->copy_error.exchange(0)) return fail(c, SN_E_HIP, c->copy_err);
+        if (take_gate_error(c))
+            return fail(c, SN_E_HIP, "swap-in gate: a DMA did not land within the gate's time limit");
+        c->rocr_run.store(rocr, std::memory_order_relaxed);
         seq = ++c->tseq;
         c->wrap_ok.store(prev_complete && c->prev_threaded);
     }
@@ -1072,6 +1203,8 @@ static int run_slabs(sn_ctx *c, int n_tok, hipStream_t cs, Pre pre, Post post, b
         hipError_t e = hipSuccess;
         if (threaded && c->sync == 1)
             e = hipStreamWaitValue64(cs, c->lflag_dev + i, seq, hipStreamWaitValueGte);
+        else if (rocr)
+            e = launch_gate(c->dsig_val[i], c->gate_limit, c->gate_err_dev, cs);
         else if (swap)
             e = hipStreamWaitEvent(cs, c->loaded[i], 0);
         if (e == hipSuccess && c->timing) e = hipEventRecord(c->t_ex0[i], cs);
@@ -1186,7 +1319,7 @@ static int capture_graphs(sn_ctx *c, const void *d_in, void *d_out) {
         if (i == 0) rc = convert_input(c, d_in, c->comp_s);
         if (!rc) rc = slab_kernels(c, i, 1, c->comp_s);
         if (!rc && i == ns - 1) rc = convert_output(c, d_out, c->comp_s);
-        if (!rc && !c->plan.resident && c->swapin == 2 && c->sync == 0) {
+        if (!rc && !c->plan.resident && c->swapin == 2 && c->sync != 1) {
             hipError_t e = launch_signal(c->sig_dev + i, c->comp_s);
             if (e != hipSuccess) rc = fail(c, SN_E_HIP, std::string("signal: ") + hipGetErrorString(e));
         }
@@ -1877,6 +2010,7 @@ extern "C" void sn_destroy(sn_ctx *c) {
         if (c->comp_s) hipStreamSynchronize(c->comp_s);
         if (c->copy_s) hipStreamSynchronize(c->copy_s);
         if (c->copy_s2) hipStreamSynchronize(c->copy_s2);
+        release_rocr_signals(c);
         for (auto *v : {&c->loaded, &c->done, &c->t_in0, &c->t_in1, &c->t_ex0, &c->t_ex1, &c->t_p0,
                         &c->t_p1, &c->t_pm})
             for (hipEvent_t e : *v)
@@ -1892,6 +2026,8 @@ extern "C" void sn_destroy(sn_ctx *c) {
         if (c->table_host) hipHostFree(c->table_host);
         if (c->sig_host) hipHostFree(c->sig_host);
         if (c->lflag_host) hipHostFree(c->lflag_host);
+        if (c->gate_err_host) hipHostFree(c->gate_err_host);
+        if (c->hsa_up) hsa_shut_down();
         for (void *p : {(void *)c->arena, (void *)c->act, (void *)c->kv, (void *)c->d_ids,
                         (void *)c->q_scratch, (void *)c->attn_ws, c->in_stage, c->out_stage,
                         (void *)c->ws})

@@ -94,6 +94,10 @@ hipError_t launch_swapin(const void *src_host_mapped, void *dst, int64_t bytes, 
 // device-mapped) once all earlier work on the stream has finished.  The host
 // polls the counter without any runtime call.
 hipError_t launch_signal(unsigned long long *flag, hipStream_t s);
+// One lane waits (at most limit_ticks of the 100 MHz real-time counter,
+// then sets *err) until *value, the value of a ROCr copy's completion
+// signal, has dropped to 0.
+hipError_t launch_gate(const int64_t *value, unsigned long long limit_ticks, int *err, hipStream_t s);
 
 hipError_t launch_embed(const int32_t *ids, const void *table, void *y, int T, int d, hipStream_t s);
 hipError_t launch_rmsnorm(const void *x, const void *gain, void *y, int T, int d, float eps,

@@ -1159,6 +1159,29 @@ hipError_t launch_signal(unsigned long long *flag, hipStream_t s) {
     return hipGetLastError();
 }
 
+// Gate of a slab whose swap-in runs on the SDMA engine through ROCr: one lane
+// polls the copy's completion signal value (1 while the copy runs, 0 once it
+// has landed) and returns when it reaches 0, so the kernels queued behind it
+// on the stream start after the copy.  The wait is bounded: after
+// `limit_ticks` of the 100 MHz real-time counter the lane sets *err and
+// returns.
+__global__ void gate_kernel(const int64_t *value, unsigned long long limit_ticks, int *err) {
+    if (threadIdx.x != 0) return;
+    const unsigned long long t0 = __builtin_amdgcn_s_memrealtime();
+    while (__hip_atomic_load(value, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_SYSTEM) > 0) {
+        if (__builtin_amdgcn_s_memrealtime() - t0 > limit_ticks) {
+            __hip_atomic_store(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+            return;
+        }
+        __builtin_amdgcn_s_sleep(2);
+    }
+}
+
+hipError_t launch_gate(const int64_t *value, unsigned long long limit_ticks, int *err, hipStream_t s) {
+    hipLaunchKernelGGL(gate_kernel, dim3(1), dim3(64), 0, s, value, limit_ticks, err);
+    return hipGetLastError();
+}
+
 // ---------------------------------------------------------------------------
 // Decoder kernels.
 // ---------------------------------------------------------------------------

@@ -283,9 +283,10 @@ def test_calibrated_searched_partition_matches_resident(name, kw, frac):
     assert rel_err(y, ref) <= TOL
 
 
-@pytest.mark.parametrize("modes", [((2, 0),), ((2, 1),), ((1, 0),), ((0, 0),),
+@pytest.mark.parametrize("modes", [((2, 0),), ((2, 1),), ((2, 2),), ((1, 0),), ((0, 0),),
                                    ((2, 0, 2),), ((2, 1, 2),),
                                    ((2, 1), (1, 0), (2, 0), (0, 0), (2, 1)),
+                                   ((2, 2), (2, 0), (1, 0), (2, 2), (2, 1), (2, 2)),
                                    ((2, 0, 2), (2, 1, 2), (2, 0, 1), (2, 0, 2), (1, 0, 2))])
 def test_back_to_back_inferences_with_cross_inference_prefetch(modes):
     # Several inferences queued without a host synchronisation: the next
@@ -293,8 +294,9 @@ def test_back_to_back_inferences_with_cross_inference_prefetch(modes):
     # the previous one still computes (waiting only for its `wrap` slabs).
     # Every output must equal a one-at-a-time inference of the same input,
     # bit for bit, in every swap-in mode (the copy thread with either kind of
-    # stream ordering, SN_OPT_SYNC 0 and 1; one DMA queue or slabs alternating
-    # between two) and when the modes alternate.
+    # stream ordering, SN_OPT_SYNC 0 and 1, or ROCr copies with gate kernels,
+    # SN_OPT_SYNC 2; one DMA queue or slabs alternating between two) and when
+    # the modes alternate.
     net, wts, x0, _ = net_case("resnet50", res=96)
     rng = np.random.default_rng(7)
     xs = [x0] + [rng.standard_normal(x0.shape).astype(np.float16) for _ in range(3)]
@@ -316,6 +318,53 @@ def test_back_to_back_inferences_with_cross_inference_prefetch(modes):
             s.synchronize()
             for i in range(len(xs)):
                 assert np.array_equal(yd[i].cpu().numpy().view(np.uint16), want[i].view(np.uint16)), (mode, i)
+
+
+@pytest.mark.parametrize("name,kw,div", [("tiny_cnn", {}, 1.0), ("resnet50", {"res": 96}, 5.81),
+                                         ("vgg16", {"res": 64}, 5.81)])
+def test_rocr_swapin_gates(tmp_path, name, kw, div):
+    # SN_OPT_SYNC 2: every swap-in is a ROCr SDMA copy with its own completion
+    # signal, and a gate kernel on the compute stream polls that signal before
+    # the slab's kernels.  Outputs equal the all-resident ones bit for bit,
+    # host and device paths, after sn_tune and sn_replan in that mode, and
+    # with an image file attached (which uses the event ordering).
+    net, wts, x0, ref = net_case(name, **kw)
+    rng = np.random.default_rng(5)
+    xs = [x0] + [rng.standard_normal(x0.shape).astype(np.float16) for _ in range(2)]
+    with S.build_engine(net, wts, budget=1 << 33) as res:
+        want = [res.infer(x) for x in xs]
+    budget = int(net.weight_bytes() * (0.6 if div == 1.0 else 1.0 / div))
+    with S.build_engine(net, wts, budget=budget) as eng:
+        eng.set_option(S.OPT_SYNC, 2)
+        st = eng.stats()
+        print(f"[case] {name}: {st['n_slabs']} slabs, budget {budget}", flush=True)
+        assert not st["resident"] and st["n_slabs"] >= 2
+        for x, w in zip(xs, want):
+            assert np.array_equal(eng.infer(x).view(np.uint16), w.view(np.uint16))
+        assert rel_err(eng.infer(x0), ref) <= TOL
+        t = eng.tune(2)
+        assert max(t) > 0
+        xd = [torch.from_numpy(x).cuda() for x in xs]
+        yd = [torch.empty(eng.out_shape, dtype=torch.float16, device="cuda") for _ in xs]
+        s = torch.cuda.Stream()
+        with torch.cuda.stream(s):
+            for rep in range(3):
+                for i in range(len(xs)):
+                    eng.infer_dev(xd[i].data_ptr(), yd[i].data_ptr(), s.cuda_stream)
+        s.synchronize()
+        for i in range(len(xs)):
+            assert np.array_equal(yd[i].cpu().numpy().view(np.uint16), want[i].view(np.uint16)), i
+        eng.replan(int(budget * 0.8))
+        assert eng.stats()["n_slabs"] >= 2
+        for x, w in zip(xs, want):
+            assert np.array_equal(eng.infer(x).view(np.uint16), w.view(np.uint16))
+        path = str(tmp_path / "image.bin")
+        eng.save_image(path)
+        eng.attach_image_file(path)
+        for sync in (2, 0, 2):
+            eng.set_option(S.OPT_SYNC, sync)
+            for x, w in zip(xs, want):
+                assert np.array_equal(eng.infer(x).view(np.uint16), w.view(np.uint16)), sync
 
 
 @pytest.mark.parametrize("name,kw", [("tiny_cnn", {}), ("resnet50", {"res": 96})])
@@ -397,7 +446,7 @@ def test_decoder_teacher_forced_parity():
     prompt = W.make_input(net)
     gen = net.extra["gen"]
     lb = sum(l.weight_bytes() for l in net.layers[1:8])
-    for budget, split, sync in ((2 * lb, None, 0), (2 * lb, None, 1), (1 << 30, 2 * lb, 0)):
+    for budget, split, sync in ((2 * lb, None, 0), (2 * lb, None, 1), (2 * lb, None, 2), (1 << 30, 2 * lb, 0)):
         eng = S.build_engine(net, wts, budget=budget, split_budget=split)
         eng.set_option(S.OPT_SYNC, sync)
         rows, fed = [], []

@@ -168,6 +168,14 @@ def test_cost_model_api_round_trip_and_errors():
     eng.set_option(S.OPT_PARTITION, 2)
     with pytest.raises(S.SwapNetError):
         eng.set_option(S.OPT_PARTITION, 3)
+    # swap-in ordering modes 0..2 (2: ROCr copies + gate kernels; a host-only
+    # context sets it up nothing)
+    for v in (2, 1, 0):
+        eng.set_option(S.OPT_SYNC, v)
+    for bad in (-1, 3):
+        with pytest.raises(S.SwapNetError) as e:
+            eng.set_option(S.OPT_SYNC, bad)
+        assert e.value.code == S.SN_E_INVALID
     eng.plan()
     lat, per = eng.predict()
     assert 0 < per <= lat * 1.5
