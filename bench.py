@@ -359,11 +359,12 @@ def conv_flops(spec, c0, c1):
     return 2.0 * ho * wo * (c1 - c0) * spec.c_in * spec.k * spec.k
 
 
-def kernel_profile(S, net, eng, torch, xd, yd):
-    """Per-kernel times of one inference (timing level 2: a HIP event pair
-    around every layer piece, plus one between a split-K convolution's main
-    kernel and its reduction), grouped by kernel.
-    Returns {name: [launches, total_ms, flops, bytes]}."""
+def kernel_profile(S, net, eng, torch, xd, yd, reps=5):
+    """Per-kernel times per inference of the swapped engine, the workload of
+    the timed loop (timing level 2: every convolution launched with start /
+    stop events of its own dispatch, a HIP event pair around every other
+    layer piece), averaged over `reps` inferences and grouped by kernel.
+    Returns {name: [launches, total_ms, flops, bytes]} per inference."""
     s = torch.cuda.current_stream()
     eng.set_option(S.OPT_TIMING, 2)
     for _ in range(2):
@@ -371,8 +372,15 @@ def kernel_profile(S, net, eng, torch, xd, yd):
         torch.cuda.synchronize()
     # the per-piece events are read back by a host-API call
     x = xd.cpu().numpy()
-    eng.infer(x)
+    runs = []
+    for _ in range(reps):
+        eng.infer(x)
+        runs.append(eng.pieces())
     eng.set_option(S.OPT_TIMING, 0)
+    pieces = runs[0]
+    for j, p in enumerate(pieces):
+        p["t_ms"] = sum(r[j]["t_ms"] for r in runs) / reps
+        p["t_main_ms"] = sum(r[j]["t_main_ms"] for r in runs) / reps
     groups = {}
 
     def add(name, t, fl, by):
@@ -381,7 +389,7 @@ def kernel_profile(S, net, eng, torch, xd, yd):
         g[1] += t
         g[2] += fl
         g[3] += by
-    for p in eng.pieces():
+    for p in pieces:
         spec = net.layers[p["layer"]]
         if spec.op == "conv2d":
             ho, wo = spec.out_hw()
@@ -722,7 +730,7 @@ def main():
         eng_sw.calibrate(5)
     model = eng_sw.cost_model()
     pred_lat, pred_per = eng_sw.predict()
-    groups = kernel_profile(S, net, eng_res, torch, xd, yr)
+    groups = kernel_profile(S, net, eng_sw, torch, xd, yd)
     conv = {k: v for k, v in groups.items() if k.startswith("conv")}
     dom = max(conv.items(), key=lambda kv: kv[1][1]) if conv else None
     total_flops = sum(v[2] for v in groups.values())

@@ -229,8 +229,9 @@ enum sn_option {
                                    with a completion signal per slab, and a
                                    one-wave gate kernel ahead of the slab's
                                    kernels polls that signal (bounded wait:
-                                   after 2 s it flags an error that the next
-                                   call reports as SN_E_HIP); "slab
+                                   after 2 s plus 1 s per GB of image it
+                                   flags an error that the next call
+                                   reports as SN_E_HIP); "slab
                                    computed" as in 0.  Runs with per-slab
                                    timing (SN_OPT_TIMING) and contexts with
                                    an image file use mode 0's ordering.

@@ -106,7 +106,7 @@ struct sn_ctx {
     std::vector<const int64_t *> dsig_val;
     int *gate_err_host = nullptr, *gate_err_dev = nullptr;
     std::atomic<bool> rocr_run{false};
-    unsigned long long gate_limit = 200000000ull;   // 2 s of the 100 MHz counter
+    unsigned long long gate_limit = 0;   // gate wait bound, ticks of the 100 MHz counter
     std::atomic<int> copy_error{0};
     std::string copy_err;
     uint8_t *act = nullptr;
@@ -267,6 +267,10 @@ static int setup_rocr_signals(sn_ctx *c) {
         *(volatile int *)c->gate_err_host = 0;
         HIP_TRY(c, hipHostGetDevicePointer((void **)&c->gate_err_dev, c->gate_err_host, 0));
     }
+    // bound of a gate's wait: 2 s plus the whole image at 1 GB/s, far above
+    // any swap-in's time on a working link (a gate waits for at most the
+    // copies queued ahead of its slab's on the SDMA engine)
+    c->gate_limit = (unsigned long long)((2.0 + (double)c->plan.image_bytes / 1e9) * 1e8);
     const int ns = (int)c->plan.slabs.size();
     c->dsig.assign(ns, hsa_signal_t{0});
     c->dsig_val.assign(ns, nullptr);
@@ -695,7 +699,10 @@ static int run_piece(sn_ctx *c, int pi, int n_tok, hipStream_t s) {
         cp.kernel = L.kernel;
         cp.ksplit = L.ksplit;
         cp.kps = L.kps;
-        e = launch_conv(cp, a, s, c->timing >= 2 ? c->t_pm[pi] : nullptr);
+        if (c->timing >= 2)
+            e = launch_conv(cp, a, s, c->t_pm[pi], c->t_p0[pi], c->t_p1[pi]);
+        else
+            e = launch_conv(cp, a, s);
         break;
     }
     case SN_OP_LINEAR: {
@@ -1051,9 +1058,11 @@ static int enqueue_copy(sn_ctx *c, int i) {
 static int slab_kernels(sn_ctx *c, int i, int n_tok, hipStream_t cs) {
     int rc;
     for (int pi : c->plan.slabs[i].pieces) {
-        if (c->timing >= 2) HIP_TRY(c, hipEventRecord(c->t_p0[pi], cs));
+        // a convolution takes its timing events from its own dispatches
+        const bool ev = c->timing >= 2 && c->layers[c->plan.pieces[pi].layer].d.op != SN_OP_CONV2D;
+        if (ev) HIP_TRY(c, hipEventRecord(c->t_p0[pi], cs));
         if ((rc = run_piece(c, pi, n_tok, cs))) return rc;
-        if (c->timing >= 2) HIP_TRY(c, hipEventRecord(c->t_p1[pi], cs));
+        if (ev) HIP_TRY(c, hipEventRecord(c->t_p1[pi], cs));
     }
     return SN_OK;
 }

@@ -71,9 +71,13 @@ ConvPlan conv_plan(int M, int N, int K, int cin_p, bool is1x1, bool allow_split,
 int64_t conv_workspace_bytes(const ConvPlan &p, int M, int N);
 int conv_kernel_count();
 const char *conv_kernel_name(int id);
-// `mid` (optional): event recorded between the split-K main kernel and its
-// reduction kernel (profiling).
-hipError_t launch_conv(const ConvPlan &p, ConvArgs a, hipStream_t s, hipEvent_t mid = nullptr);
+// `mid` (optional) is recorded between a K-split convolution's main kernel
+// and its reduction.  With `t0` and `t1` (per-piece timing) the kernels are
+// launched with start / stop events taken from their own dispatches: t0 at
+// the main kernel's start, `mid` (K split) at its end, t1 at the end of the
+// last kernel, so that t0 .. t1 is execution time without event overhead.
+hipError_t launch_conv(const ConvPlan &p, ConvArgs a, hipStream_t s, hipEvent_t mid = nullptr,
+                       hipEvent_t t0 = nullptr, hipEvent_t t1 = nullptr);
 hipError_t launch_gemv(const GemvArgs &a, hipStream_t s);
 
 hipError_t launch_maxpool(const void *x, void *y, int H, int W, int Cp, int Ho, int Wo, int k,

@@ -11,6 +11,8 @@
 // tree); splitting a layer by output channels never changes any output bit.
 #include "kernels.h"
 
+#include <hip/hip_ext.h>
+
 #include <math.h>
 
 #include <algorithm>
@@ -841,7 +843,8 @@ int64_t conv_workspace_bytes(const ConvPlan &p, int M, int N) {
 }
 
 
-hipError_t launch_conv(const ConvPlan &p, ConvArgs a, hipStream_t s, hipEvent_t mid) {
+hipError_t launch_conv(const ConvPlan &p, ConvArgs a, hipStream_t s, hipEvent_t mid, hipEvent_t t0,
+                       hipEvent_t t1) {
     if (p.kernel < 0 || p.kernel >= kNumConvVariants) return hipErrorInvalidValue;
     const ConvVariant &v = kConvVariants[p.kernel];
     if (a.M <= 0 || a.N <= 0) return hipSuccess;
@@ -853,12 +856,22 @@ hipError_t launch_conv(const ConvPlan &p, ConvArgs a, hipStream_t s, hipEvent_t 
         return hipErrorInvalidValue;
     a.n_cover = std::max(a.N, a.n_zero_end - a.n0);
     long blocks = (long)((a.M + v.bm - 1) / v.bm) * ((a.n_cover + v.bn - 1) / v.bn);
-    hipLaunchKernelGGL(v.fn, dim3((unsigned)blocks, (unsigned)a.ksplit), dim3(v.threads), 0, s, a);
+    const dim3 grid((unsigned)blocks, (unsigned)a.ksplit);
+    const long n = (long)a.M * ((a.n_cover + 3) / 4);
+    const dim3 rgrid((unsigned)((n + 255) / 256));
+    if (t0 && t1) {
+        // timing: events from the kernels' own dispatches
+        hipExtLaunchKernelGGL(v.fn, grid, dim3(v.threads), 0, s, t0, a.ksplit == 1 ? t1 : mid, 0, a);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess || a.ksplit == 1) return e;
+        hipExtLaunchKernelGGL(splitk_reduce_kernel, rgrid, dim3(256), 0, s, nullptr, t1, 0, a);
+        return hipGetLastError();
+    }
+    hipLaunchKernelGGL(v.fn, grid, dim3(v.threads), 0, s, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || a.ksplit == 1) return e;
     if (mid && (e = hipEventRecord(mid, s)) != hipSuccess) return e;
-    long n = (long)a.M * ((a.n_cover + 3) / 4);
-    hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(splitk_reduce_kernel, rgrid, dim3(256), 0, s, a);
     return hipGetLastError();
 }
 
