@@ -255,6 +255,15 @@ enum sn_option {
                                    variant's kind (1x1 / token GEMM, taps
                                    with Cin_p % 64 == 0, or general).  Set
                                    before sn_plan (or before sn_replan)       */
+    SN_OPT_GATE_LIMIT_US = 12,  /* failure tests only: bound of each gate
+                                   kernel's wait (SN_OPT_SYNC 2) in
+                                   microseconds; 0 (default) = 2 s plus 1 s
+                                   per GB of image.  A gate that runs out
+                                   lets its slab's kernels start before the
+                                   slab has landed (their output is then
+                                   undefined) and the next call reports
+                                   SN_E_HIP.  May be set after plan,
+                                   between inferences                         */
     SN_OPT_GRAPH = 4            /* 1 (default): the kernels of each slab of an
                                    image network are captured once per
                                    (input, output) buffer pair into one HIP

@@ -107,6 +107,7 @@ struct sn_ctx {
     int *gate_err_host = nullptr, *gate_err_dev = nullptr;
     std::atomic<bool> rocr_run{false};
     unsigned long long gate_limit = 0;   // gate wait bound, ticks of the 100 MHz counter
+    int64_t gate_limit_us = 0;           // SN_OPT_GATE_LIMIT_US (0: the plan's bound)
     std::atomic<int> copy_error{0};
     std::string copy_err;
     uint8_t *act = nullptr;
@@ -430,6 +431,12 @@ extern "C" int sn_set_option(sn_ctx *c, int option, int64_t value) {
         if (value < 0 || value > conv_kernel_count())
             return fail(c, SN_E_INVALID, "conv kernel configuration out of range");
         c->conv_force = (int)value;
+        return SN_OK;
+    case SN_OPT_GATE_LIMIT_US:
+        if (value < 0 || value > 3600ll * 1000000ll)
+            return fail(c, SN_E_INVALID, "gate limit must be in [0, 1 h] (microseconds)");
+        if (c->state == ST_PLANNED && c->have_prev) wait_copier_idle(c);
+        c->gate_limit_us = value;
         return SN_OK;
     default:
         return fail(c, SN_E_INVALID, "unknown option");
@@ -1213,7 +1220,9 @@ static int run_slabs(sn_ctx *c, int n_tok, hipStream_t cs, Pre pre, Post post, b
         if (threaded && c->sync == 1)
             e = hipStreamWaitValue64(cs, c->lflag_dev + i, seq, hipStreamWaitValueGte);
         else if (rocr)
-            e = launch_gate(c->dsig_val[i], c->gate_limit, c->gate_err_dev, cs);
+            e = launch_gate(c->dsig_val[i],
+                            c->gate_limit_us > 0 ? (unsigned long long)c->gate_limit_us * 100ull : c->gate_limit,
+                            c->gate_err_dev, cs);
         else if (swap)
             e = hipStreamWaitEvent(cs, c->loaded[i], 0);
         if (e == hipSuccess && c->timing) e = hipEventRecord(c->t_ex0[i], cs);

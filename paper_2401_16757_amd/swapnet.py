@@ -32,6 +32,7 @@ OPT_PARTITION = 8
 OPT_SYNC = 9
 OPT_NAIVE = 10
 OPT_CONV_KERNEL = 11
+OPT_GATE_LIMIT_US = 12
 NAIVE_SEQUENTIAL, NAIVE_ALLOC, NAIVE_PAGEABLE, NAIVE_COPY_ASSEMBLY = 1, 2, 4, 8
 
 EXPORTS = ["sn_create", "sn_create_ex", "sn_add_block", "sn_plan", "sn_set_option", "sn_infer",

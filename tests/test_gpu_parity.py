@@ -367,6 +367,28 @@ def test_rocr_swapin_gates(tmp_path, name, kw, div):
                 assert np.array_equal(eng.infer(x).view(np.uint16), w.view(np.uint16)), sync
 
 
+def test_gate_time_out_is_reported():
+    # Failure path of the device-side gates (SN_OPT_SYNC 2), forced from the
+    # host: with a 1 us bound every gate that starts before its slab has
+    # landed gives up at once.  VGG-16 at 1/5.81 is link-bound (12 slabs of
+    # ~23 MB, ~0.4 ms each, little compute), so gates do start early.  The
+    # call reports SN_E_HIP (its output is undefined), the error is reported
+    # once, and with the bound restored the outputs are bit-identical again.
+    net, wts, x0, _ = net_case("vgg16")
+    with S.build_engine(net, wts, budget=int(net.weight_bytes() / 5.81)) as eng:
+        st = eng.stats()
+        print(f"[case] vgg16 gate time-out: {st['n_slabs']} slabs", flush=True)
+        want = eng.infer(x0)
+        eng.set_option(S.OPT_GATE_LIMIT_US, 1)
+        with pytest.raises(S.SwapNetError) as e:
+            for _ in range(3):
+                eng.infer(x0)
+        assert e.value.code == S.SN_E_HIP and "gate" in str(e.value)
+        eng.set_option(S.OPT_GATE_LIMIT_US, 0)
+        for _ in range(2):
+            assert np.array_equal(eng.infer(x0).view(np.uint16), want.view(np.uint16))
+
+
 @pytest.mark.parametrize("name,kw", [("tiny_cnn", {}), ("resnet50", {"res": 96})])
 def test_image_file_swapin_matches_memory(tmp_path, name, kw):
     # Storage tier (direct block fetch): after sn_attach_image_file every

@@ -176,6 +176,12 @@ def test_cost_model_api_round_trip_and_errors():
         with pytest.raises(S.SwapNetError) as e:
             eng.set_option(S.OPT_SYNC, bad)
         assert e.value.code == S.SN_E_INVALID
+    for v in (1, 0):
+        eng.set_option(S.OPT_GATE_LIMIT_US, v)
+    for bad in (-1, 3600 * 10**6 + 1):
+        with pytest.raises(S.SwapNetError) as e:
+            eng.set_option(S.OPT_GATE_LIMIT_US, bad)
+        assert e.value.code == S.SN_E_INVALID
     eng.plan()
     lat, per = eng.predict()
     assert 0 < per <= lat * 1.5
