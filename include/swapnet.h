@@ -337,14 +337,19 @@ int sn_get_cost_model(const sn_ctx *ctx, sn_cost_model *out, float *layer_ex, in
  * (what sn_get_cost_model then returns; gamma and kappa are kept):
  *  - alpha, beta: X = min(image, budget) bytes of the image copied into the
  *    arena as one DMA and as 16 DMAs with an event after each (beta = the
- *    extra time per DMA, alpha = the rest per byte; best of `reps`);
+ *    extra time per DMA, alpha = the rest per byte; best of `reps`); with
+ *    SN_OPT_SYNC 2 (no image file) the same copies are then issued as the
+ *    engine issues them, through ROCr with a completion signal, timed on
+ *    the host from the first issue to the last completion, and kept;
  *  - layer_ex: per-piece events (timing level 2), median of `reps`
  *    inferences; for image networks then scaled, slab by slab, to the time
  *    of the slab's captured graph replayed without swap-ins, so that they
  *    include the per-slab overhead (slab_ex is then 0);
- *  - swapped plans: wake from per-slab events (timing level 1), and gate
- *    fitted (in [0, 1 ms]) so that the model's time per inference equals the
- *    measured one for 8 inferences issued back to back.
+ *  - swapped plans: wake from per-slab events (timing level 1); with
+ *    SN_OPT_SYNC 2 instead what a gate kernel on a completed copy's signal
+ *    adds ahead of the next kernel (two gates against one); gate fitted (in
+ *    [0, 1 ms]) so that the model's time per inference equals the measured
+ *    one for 8 inferences issued back to back.
  * The inferences run on the staging buffers (image networks, zero input) or
  * with token id 0 at the current position, which is not advanced (token
  * networks: the KV entry at that position is overwritten; needs position <
@@ -357,10 +362,13 @@ int sn_calibrate(sn_ctx *ctx, int reps);
 /* Choose the partition by measurement: calibrate the delay model on the
  * current plan (as sn_calibrate), then plan the context in place
  * (sn_replan) with each of SN_OPT_PARTITION 0, 1 and 2 (the last searched
- * under the fresh model), time 8 inferences issued back to back for each
- * (best of max(1, reps / 2) rounds) and keep the fastest; SN_OPT_PARTITION
- * is left at the chosen value.  `times_s` (NULL or 3 doubles) receives the
- * measured seconds per inference of partitions 0, 1, 2 (0: infeasible).  A
+ * under the fresh model; with SN_OPT_SYNC 2 searched twice, under the model
+ * measured on the ROCr path and under the one measured with events), time
+ * 8 inferences issued back to back for each (best of max(1, reps / 2)
+ * rounds) and keep the fastest plan and its model; SN_OPT_PARTITION is
+ * left at the chosen value.  `times_s` (NULL or 3 doubles) receives the
+ * measured seconds per inference of partitions 0, 1, 2 (the faster of the
+ * two searches for 2; 0: infeasible).  A
  * resident plan is left as it is.  Runs inferences as sn_calibrate does.
  * Errors: as sn_calibrate and sn_replan. */
 int sn_tune(sn_ctx *ctx, int reps, double *times_s);

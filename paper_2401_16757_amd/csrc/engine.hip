@@ -1675,7 +1675,11 @@ static int calib_run(sn_ctx *c) {
 // events scaled to the slab graphs' own times, the wake latency from
 // per-slab events, and the gate latency fitted to the measured time per
 // inference of this plan.  The steps are described with sn_calibrate.
-static int calibrate_impl(sn_ctx *c, int reps, CostModel &m) {
+static int calibrate_impl(sn_ctx *c, int reps, CostModel &m, CostModel *alt = nullptr, bool *have_alt = nullptr) {
+    if (have_alt) *have_alt = false;
+    // with ROCr swap-ins the model's DMA terms are measured on that path;
+    // the event path's values are kept for `alt` (sn_tune tries both)
+    double ev_alpha = -1, ev_beta = -1, ev_wake = -1;
     HIP_TRY(c, ensure_stream(&c->comp_s));
     HIP_TRY(c, ensure_own_queue_stream(&c->copy_s, c->device));
     if (c->copier.joinable()) wait_copier_idle(c);
@@ -1720,6 +1724,40 @@ static int calibrate_impl(sn_ctx *c, int reps, CostModel &m) {
         }
         m.beta = std::max(0.0, (t_many - t_one) / (K - 1));
         m.alpha = std::max(t_one - m.beta, 0.5 * t_one) / (double)X;
+        ev_alpha = m.alpha;
+        ev_beta = m.beta;
+        // the engine's own swap-ins go through ROCr (SN_OPT_SYNC 2): the
+        // per-DMA cost is that of those copies, each with its signal
+        // decrement and no event, timed on the host from the first issue to
+        // the last completion
+        if (c->sync == 2 && c->img_fd < 0 && !c->dsig.empty()) {
+            const hsa_signal_t sg = c->dsig[0];
+            auto rocr_chain = [&](int n, double &t) -> bool {
+                const int64_t each = X / n;
+                hsa_signal_store_relaxed(sg, n);
+                const auto t0 = std::chrono::steady_clock::now();
+                for (int k = 0; k < n; ++k)
+                    if (hsa_amd_memory_async_copy(c->arena + k * each, c->hsa_gpu, c->image + k * each,
+                                                  c->hsa_cpu, (size_t)each, 0, nullptr, sg) != HSA_STATUS_SUCCESS) {
+                        hsa_signal_store_relaxed(sg, 0);
+                        return false;
+                    }
+                hsa_signal_wait_scacquire(sg, HSA_SIGNAL_CONDITION_LT, 1, UINT64_MAX, HSA_WAIT_STATE_ACTIVE);
+                t = std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count();
+                return true;
+            };
+            double r_one = 0, r_many = 0;
+            bool ok = true;
+            for (int r = 0; r < reps && ok; ++r) {
+                double a = 0, b = 0;
+                ok = rocr_chain(1, a) && rocr_chain(K, b);
+                r_one = r ? std::min(r_one, a) : a;
+                r_many = r ? std::min(r_many, b) : b;
+            }
+            if (!ok) return fail(c, SN_E_HIP, "calibration: hsa_amd_memory_async_copy failed");
+            m.beta = std::max(0.0, (r_many - r_one) / (K - 1));
+            m.alpha = std::max(r_one - m.beta, 0.5 * r_one) / (double)X;
+        }
     }
 
     // execution: per layer, from per-piece events
@@ -1765,6 +1803,28 @@ static int calibrate_impl(sn_ctx *c, int reps, CostModel &m) {
             }
         }
         if (!rc && !wake.empty()) m.wake = median_of(wake);
+        ev_wake = m.wake;
+        // on the ROCr path a slab's kernels wait behind a gate kernel rather
+        // than an event: wake = what a gate adds ahead of the next kernel
+        // once its copy has landed (two gates against one on a signal at 0;
+        // best of `reps`)
+        if (!rc && c->sync == 2 && c->img_fd < 0 && !c->dsig.empty()) {
+            hsa_signal_store_relaxed(c->dsig[0], 0);
+            double g1 = 1e30, g2 = 1e30;
+            for (int r = 0; r < std::max(reps, 3) && !rc; ++r)
+                for (int n = 1; n <= 2 && !rc; ++n) {
+                    hipError_t e = hipEventRecord(c->t_start, c->comp_s);
+                    for (int k = 0; k < n && e == hipSuccess; ++k)
+                        e = launch_gate(c->dsig_val[0], c->gate_limit, c->gate_err_dev, c->comp_s);
+                    if (e == hipSuccess) e = hipEventRecord(c->t_ex0[0], c->comp_s);
+                    if (e == hipSuccess) e = hipStreamSynchronize(c->comp_s);
+                    float ms = 0;
+                    if (e == hipSuccess) e = hipEventElapsedTime(&ms, c->t_start, c->t_ex0[0]);
+                    if (e != hipSuccess) rc = fail(c, SN_E_HIP, std::string("calibration: ") + hipGetErrorString(e));
+                    (n == 1 ? g1 : g2) = std::min(n == 1 ? g1 : g2, ms * 1e-3);
+                }
+            if (!rc) m.wake = std::max(0.0, g2 - g1);
+        }
     }
     c->timing = saved;
 
@@ -1831,23 +1891,36 @@ static int calibrate_impl(sn_ctx *c, int reps, CostModel &m) {
             float ms = 0;
             HIP_TRY(c, hipEventElapsedTime(&ms, c->t_start, c->t_ex0[0]));
             const double P = ms * 1e-3 / K;
-            auto period_at = [&](double g) {
-                CostModel t = m;
-                t.gate = g;
-                return simulate_plan(c->layers, c->plan, t).period;
-            };
-            double lo = 0, hi = 1e-3;
-            if (period_at(lo) >= P) {
-                m.gate = 0;
-            } else if (period_at(hi) <= P) {
-                m.gate = hi;
-            } else {
-                for (int it = 0; it < 40; ++it) {
-                    const double mid = 0.5 * (lo + hi);
-                    if (period_at(mid) < P) lo = mid;
-                    else hi = mid;
+            // the gate that makes model `mm` reproduce the measured period
+            auto fit_gate = [&](CostModel &mm) {
+                auto period_at = [&](double g) {
+                    CostModel t = mm;
+                    t.gate = g;
+                    return simulate_plan(c->layers, c->plan, t).period;
+                };
+                double lo = 0, hi = 1e-3;
+                if (period_at(lo) >= P) {
+                    mm.gate = 0;
+                } else if (period_at(hi) <= P) {
+                    mm.gate = hi;
+                } else {
+                    for (int it = 0; it < 40; ++it) {
+                        const double mid = 0.5 * (lo + hi);
+                        if (period_at(mid) < P) lo = mid;
+                        else hi = mid;
+                    }
+                    mm.gate = 0.5 * (lo + hi);
                 }
-                m.gate = 0.5 * (lo + hi);
+            };
+            fit_gate(m);
+            const bool differs = ev_beta >= 0 && ev_wake >= 0 && (ev_beta != m.beta || ev_wake != m.wake);
+            if (alt && have_alt && differs) {
+                *alt = m;
+                alt->alpha = ev_alpha;
+                alt->beta = ev_beta;
+                alt->wake = ev_wake;
+                fit_gate(*alt);
+                *have_alt = true;
             }
         }
     }
@@ -1889,14 +1962,22 @@ extern "C" int sn_tune(sn_ctx *c, int reps, double *times_s) {
         for (int p = 0; p < 3; ++p) times_s[p] = 0;
     if (c->plan.resident) return SN_OK;
     HIP_TRY(c, ensure_stream(&c->comp_s));
-    CostModel m = c->cost;
-    if ((rc = calibrate_impl(c, reps, m))) return rc;
+    CostModel m = c->cost, alt;
+    bool have_alt = false;
+    if ((rc = calibrate_impl(c, reps, m, &alt, &have_alt))) return rc;
     c->cost = m;
     const int orig = c->partition;
     int best = -1;
     double best_t = 0;
-    for (int p = 0; p < 3; ++p) {
+    // partition 2 is searched under the model measured on the engine's own
+    // swap-in path and, with ROCr swap-ins, also under the event path's
+    // (the two search differently); the faster plan and its model are kept
+    const int n_try = have_alt ? 4 : 3;
+    int best_model = 0;   // 0: m, 1: alt (partition 2 only)
+    for (int k = 0; k < n_try; ++k) {
+        const int p = std::min(k, 2);
         c->partition = p;
+        c->cost = k == 3 ? alt : m;
         rc = sn_replan(c, 0);
         if (rc == SN_E_INFEASIBLE) continue;
         if (rc) return rc;
@@ -1907,14 +1988,18 @@ extern "C" int sn_tune(sn_ctx *c, int reps, double *times_s) {
             t = r ? std::min(t, x) : x;
         }
         if (rc) return rc;
-        if (times_s) times_s[p] = t;
+        if (times_s && (times_s[p] == 0 || t < times_s[p])) times_s[p] = t;
         if (best < 0 || t < best_t) {
             best = p;
             best_t = t;
+            best_model = k == 3 ? 1 : 0;
         }
     }
     c->partition = best >= 0 ? best : orig;
-    if (c->partition != 2) return sn_replan(c, 0);
+    c->cost = best_model ? alt : m;
+    // the last plan made is that of the last candidate tried
+    const bool last_is_best = c->partition == 2 && best_model == (n_try == 4 ? 1 : 0);
+    if (!last_is_best) return sn_replan(c, 0);
     return SN_OK;
 }
 
